@@ -1,0 +1,259 @@
+#!/usr/bin/env python3
+"""Benchmark of the decode-maximal hybrid-batch decoder layer on one MI355X.
+
+A step is one pass of the whole hot path -- one decoder layer over one
+hybrid batch (norm_1, preproj, rotary embedding + KV append, chunk and
+decode attention, postproj, norm_2, ffn_ln1, ffn_ln2), through the C-ABI --
+over synthetic, seeded inputs already resident in HBM.  Default workload:
+a LLaMA-13B-shaped layer, chunk 256 at offset 512 + 64 decodes with context
+uniform in [256, 1024] (T = 320 rows), bf16.
+
+Prints ONE JSON line: hybrid tokens/s (value), the decode accounting of the
+paper (Sec. 5.1.1) from prefill-only and decode-only runs of the same rows,
+per-stage times from HIP events recorded on the launch stream inside the
+timed region, the roofline of the dominant kernel and the oracle timed on
+the host cores (cpu_baseline).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3
+PEAK_HBM_GBPS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="llama13b-layer-bf16-c256-b64")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-compare", action="store_true", help="skip the prefill-only / decode-only runs")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 1 GiB elementwise copy kernel (for HBM counter scaling)")
+    return ap.parse_args()
+
+
+def stage_work(shp, b, S_stats=None):
+    """Algorithmic FLOPs and HBM bytes of each stage of one layer call.
+
+    Bytes count what the method must move once: weights once, KV read once
+    per query set, activations once in and once out; FLOPs count 2 per
+    multiply-add, attention pairs only where the mask allows them."""
+    T, C, B = b.n_tokens, b.chunk_len, b.n_decodes
+    H, nh, hd, F = shp.hidden, shp.n_heads, shp.head_dim, shp.ffn
+    QD = nh * hd
+    es = 2 if shp.dtype == "bf16" else 4
+    up_rows = 2 * F if shp.act == "swiglu" else F
+    ctx = [int(c) for c in b.decode_ctx]
+    dec_keys = sum(c + 1 for c in ctx)
+    pre_pairs = C * b.chunk_offset + C * (C + 1) // 2
+    pre_keys = b.chunk_offset + C if C else 0
+    w = {}
+    w["norm_1"] = (0.0, 2 * T * H * es + T * H * 4)
+    w["preproj"] = (2.0 * T * H * 3 * QD, 3 * QD * H * es + T * H * es + T * 3 * QD * es)
+    w["rope_kv_append"] = (0.0, 2 * T * 3 * QD * es + T * QD * es)
+    w["chunk_attention"] = (4.0 * pre_pairs * hd * nh, pre_keys * 2 * QD * es + 2 * C * QD * es)
+    w["decode_attention"] = (4.0 * dec_keys * hd * nh, dec_keys * 2 * QD * es + 2 * B * QD * es)
+    w["postproj"] = (2.0 * T * QD * H, H * QD * es + T * QD * es + T * H * es + T * H * 4)
+    w["norm_2"] = (0.0, T * H * 4 + T * H * es + T * H * 4)
+    w["ffn_ln1"] = (2.0 * T * H * up_rows, up_rows * H * es + T * H * es + T * F * es)
+    w["ffn_ln2"] = (2.0 * T * F * H, H * F * es + T * F * es + T * H * 4 + T * H * es)
+    return w
+
+
+BOUND = {"norm_1": "hbm", "preproj": "mfma", "rope_kv_append": "hbm", "chunk_attention": "mfma",
+         "decode_attention": "hbm", "postproj": "mfma", "norm_2": "hbm", "ffn_ln1": "mfma", "ffn_ln2": "mfma"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: the hot path runs on a single MI355X and has no multi-GPU mode "
+              f"(asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import workloads as wl
+    from paper_2308_16369_amd import sarathi as S
+    from paper_2308_16369_amd import accounting
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    w = wl.WORKLOADS[args.workload]
+    shp = w.shape
+    t0 = time.time()
+    inst = wl.generate(w)
+    print(f"# generated {w.name} in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+    b = inst.batch
+    T, C, B = b.n_tokens, b.chunk_len, b.n_decodes
+
+    def dev(a):
+        if shp.dtype == "bf16":
+            return torch.from_numpy(wl.bf16_bits(a).view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda()
+
+    cfg = S.make_cfg(hidden=shp.hidden, n_heads=shp.n_heads, head_dim=shp.head_dim, ffn=shp.ffn, n_layers=1,
+                     norm=S.NORM_RMS if shp.norm == "rms" else S.NORM_LAYER,
+                     act=S.ACT_SWIGLU if shp.act == "swiglu" else S.ACT_GELU, rope=int(shp.rope),
+                     rope_base=shp.rope_base, eps=shp.eps, dtype=S.BF16 if shp.dtype == "bf16" else S.F32)
+    wdev = {k: dev(v) for k, v in inst.weights[0].items()}
+    wabi = S.make_weights({k: t.data_ptr() for k, t in wdev.items()})
+    kv_t = dev(inst.kv)
+    Sx = kv_t.shape[4]
+    kv = S.sarathi_kv_alloc(cfg, kv_t.shape[1], Sx, kv_t.data_ptr(), kv_t.numel() * kv_t.element_size())
+    ws_bytes = S.sarathi_workspace_bytes(cfg, T, B, Sx)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    x = dev(inst.x)
+    y = torch.empty_like(x)
+    stream = torch.cuda.current_stream()
+    print(f"# uploaded in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+
+    def run(batch, xin, xout, steps, warmup, profile=False):
+        bb, keep = S.make_batch(batch.prefill_slot, batch.chunk_offset, batch.chunk_len,
+                                list(batch.decode_slots), list(batch.decode_ctx))
+        call = lambda: S.sarathi_hybrid_layer_forward(cfg, wabi, kv, 0, bb, xin.data_ptr(), xout.data_ptr(),
+                                                      ws.data_ptr(), ws_bytes, stream.cuda_stream)
+        for _ in range(warmup):
+            call()
+        torch.cuda.synchronize()
+        if profile:
+            S.sarathi_profile_begin(steps)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t_wall = time.perf_counter()
+        e0.record(stream)
+        for _ in range(steps):
+            call()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t_wall
+        stages = None
+        if profile:
+            stages, n = S.sarathi_profile_end()
+            stages = {k: v / n for k, v in stages.items()}
+        return e0.elapsed_time(e1) / steps, wall / steps * 1e3, stages
+
+    # ---- timed region: K hybrid steps, with per-stage HIP events on the launch stream
+    ms, wall_ms, stages = run(b, x, y, args.steps, args.warmup, profile=True)
+    # ---- same steps without the stage events (the events' own cost)
+    ms_plain, _, _ = run(b, x, y, args.steps, 2)
+    print(f"# hybrid: {ms:.4f} ms/step with stage events, {ms_plain:.4f} without", file=sys.stderr, flush=True)
+
+    # ---- decode accounting (Sec. 5.1.1): prefill-only and decode-only batches of the same rows
+    extra = {}
+    if not args.no_compare and C > 0 and B > 0:
+        bp = wl.Batch(b.prefill_slot, b.chunk_offset, C, np.zeros(0, np.int32), np.zeros(0, np.int32))
+        bd = wl.Batch(-1, 0, 0, b.decode_slots, b.decode_ctx)
+        xp, yp = x[:C].clone(), torch.empty_like(x[:C])
+        xd, yd = x[C:].clone(), torch.empty_like(x[C:])
+        ms_p, _, _ = run(bp, xp, yp, args.steps, 2)
+        ms_d, _, _ = run(bd, xd, yd, args.steps, 2)
+        t_dec_h = accounting.decode_time_per_token_hybrid(ms_plain, ms_p, B)
+        t_dec_b = accounting.decode_time_per_token_baseline(ms_d, B)
+        extra = {
+            "prefill_only_ms": round(ms_p, 5), "decode_only_ms": round(ms_d, 5),
+            "decode_tokens_per_s_hybrid": round(1e3 / t_dec_h, 1) if t_dec_h > 0 else None,
+            "decode_tokens_per_s_decode_only": round(1e3 / t_dec_b, 1),
+            "decode_speedup": round(t_dec_b / t_dec_h, 3) if t_dec_h > 0 else None,
+        }
+
+    if args.copy_calibration:
+        a = torch.empty(1 << 29, dtype=torch.float16, device="cuda").fill_(1.0)   # 1 GiB
+        c = torch.empty_like(a)
+        for _ in range(3):
+            torch.mul(a, 1.0, out=c)
+        torch.cuda.synchronize()
+        del a, c
+
+    # ---- rooflines per stage
+    work = stage_work(shp, b)
+    peak_flops = PEAK_BF16_TFLOPS if shp.dtype == "bf16" else PEAK_F32_TFLOPS
+    kernels = {}
+    for name, t in stages.items():
+        fl, by = work[name]
+        sec = t * 1e-3
+        if sec <= 0:
+            continue
+        tf = fl / sec / 1e12
+        gb = by / sec / 1e9
+        kernels[name] = {"ms": round(t, 5), "tflops": round(tf, 2), "gbps": round(gb, 1),
+                         "mfma_frac": round(tf / peak_flops, 4), "hbm_frac": round(gb / PEAK_HBM_GBPS, 4),
+                         "bound": BOUND[name]}
+    dom = max(kernels, key=lambda k: kernels[k]["ms"])
+    dk = kernels[dom]
+    if dk["bound"] == "mfma":
+        roof = {"bound": "mfma", "achieved": dk["tflops"], "peak": peak_flops, "unit": "TFLOP/s",
+                "frac": dk["mfma_frac"]}
+    else:
+        roof = {"bound": "hbm", "achieved": dk["gbps"], "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                "frac": dk["hbm_frac"]}
+    roof["kernel"] = dom
+    roof["traffic"] = None
+    lin = ["preproj", "postproj", "ffn_ln1", "ffn_ln2"]
+    lin_ms = sum(kernels[k]["ms"] for k in lin if k in kernels)
+    lin_flops = sum(work[k][0] for k in lin)
+    lin_bytes = sum(work[k][1] for k in lin)
+
+    # ---- oracle on the host cores, bounded sample: one full layer call (all T rows)
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        from threadpoolctl import threadpool_info
+        ob = oracle.OracleBatch(b.prefill_slot, b.chunk_offset, C, list(b.decode_slots), list(b.decode_ctx))
+        times = []
+        t_start = time.perf_counter()
+        while len(times) < 3 and (time.perf_counter() - t_start) < 25.0:
+            kvc = inst.kv[0]
+            t1 = time.perf_counter()
+            oracle.layer_forward(shp, inst.weights[0], kvc.copy() if not times else kvc, ob, inst.x)
+            times.append(time.perf_counter() - t1)
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"],
+                           default=1)
+        t_cpu = float(np.median(times))
+        cpu = {"value": round(T / t_cpu, 2), "unit": "tokens/s", "cores": int(blas_threads), "kind": "oracle",
+               "sample": f"one full layer call of the same workload ({T} rows), float64 NumPy, median of "
+                         f"{len(times)} runs of {t_cpu:.2f}s; host affinity {len(os.sched_getaffinity(0))} cpus"}
+
+    value = T / (ms_plain * 1e-3)
+    line = {
+        "metric": "hybrid-batch tokens/s per layer (C+B rows per layer forward)",
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_plain, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": shp.dtype,
+        "data": "synthetic (seeded N(0,1) activations/KV, N(0,0.02) weights; no trained weights)",
+        "config": {"workload": w.name, "hidden": shp.hidden, "heads": shp.n_heads, "head_dim": shp.head_dim,
+                   "ffn": shp.ffn, "chunk_len": C, "chunk_offset": b.chunk_offset, "n_decodes": B,
+                   "ctx_range": [w.batch.ctx_lo, w.batch.ctx_hi], "rows": T, "parallelism": "none (1 GPU)"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "ms_per_step_with_stage_events": round(ms, 5),
+        "wall_ms_per_step": round(wall_ms, 5),
+        "linear_ops": {"ms": round(lin_ms, 5), "mfma_frac": round(lin_flops / (lin_ms * 1e-3) / 1e12 / peak_flops, 4),
+                       "weight_stream_hbm_frac": round(lin_bytes / (lin_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)},
+        "kernels": kernels,
+        **extra,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,184 @@
+// The "others" ops of the decoder block (norms, rotary embedding + KV append,
+// casts) and the batch-metadata writer.  All memory-bound; one pass each.
+#include "kernels.h"
+
+namespace sarathi {
+
+// ------------------------------------------------------------------ metadata
+__global__ void meta_write_kernel(MetaChunk c, int* dst) {
+  for (int i = threadIdx.x; i < c.count; i += blockDim.x) dst[i] = c.values[i];
+}
+
+hipError_t launch_meta_write(const MetaChunk& chunk, int* dst, hipStream_t s) {
+  hipLaunchKernelGGL(meta_write_kernel, dim3(1), dim3(256), 0, s, chunk, dst);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ norms
+// Block-wide sum over 256 threads (4 waves).
+__device__ __forceinline__ float block_sum_256(float v, float* red) {
+  v = wave_sum(v);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  return red[0] + red[1] + red[2] + red[3];
+}
+
+// One row per block.  RMS: x / sqrt(mean(x^2) + eps) * g.
+// LayerNorm: (x - mean) / sqrt(mean((x - mean)^2) + eps) * g + b.
+template <typename Tin, typename Tout, bool LAYER>
+__global__ __launch_bounds__(256) void norm_kernel(const Tin* __restrict__ in, const Tout* __restrict__ g,
+                                                   const Tout* __restrict__ b, Tout* __restrict__ out,
+                                                   float* __restrict__ copy_f32, int H, float eps) {
+  __shared__ float red[4];
+  const size_t row = blockIdx.x;
+  const Tin* x = in + row * (size_t)H;
+  constexpr int E = Vec16<Tin>::N;
+  const int nchunk = H / E;
+  float mean = 0.f;
+  if (LAYER) {
+    float s = 0.f;
+    for (int c = threadIdx.x; c < nchunk; c += 256) {
+      float f[E];
+      Vec16<Tin>::unpack(reinterpret_cast<const uint4*>(x)[c], f);
+#pragma unroll
+      for (int e = 0; e < E; ++e) s += f[e];
+    }
+    mean = block_sum_256(s, red) / (float)H;
+  }
+  float ss = 0.f;
+  for (int c = threadIdx.x; c < nchunk; c += 256) {
+    float f[E];
+    Vec16<Tin>::unpack(reinterpret_cast<const uint4*>(x)[c], f);
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const float d = f[e] - mean;
+      ss += d * d;
+    }
+  }
+  const float r = 1.0f / sqrtf(block_sum_256(ss, red) / (float)H + eps);
+  Tout* y = out + row * (size_t)H;
+  for (int c = threadIdx.x; c < nchunk; c += 256) {
+    float f[E];
+    Vec16<Tin>::unpack(reinterpret_cast<const uint4*>(x)[c], f);
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const int i = c * E + e;
+      float v = (f[e] - mean) * r * to_f<Tout>(g[i]);
+      if (LAYER) v += to_f<Tout>(b[i]);
+      y[i] = from_f<Tout>(v);
+      if (copy_f32) copy_f32[row * (size_t)H + i] = f[e];
+    }
+  }
+}
+
+template <typename Tin, typename Tout>
+static void norm_dispatch(bool layer, const void* in, const void* g, const void* b, void* out,
+                          float* copy_f32, int rows, int H, float eps, hipStream_t s) {
+  if (layer)
+    hipLaunchKernelGGL((norm_kernel<Tin, Tout, true>), dim3(rows), dim3(256), 0, s, (const Tin*)in,
+                       (const Tout*)g, (const Tout*)b, (Tout*)out, copy_f32, H, eps);
+  else
+    hipLaunchKernelGGL((norm_kernel<Tin, Tout, false>), dim3(rows), dim3(256), 0, s, (const Tin*)in,
+                       (const Tout*)g, (const Tout*)b, (Tout*)out, copy_f32, H, eps);
+}
+
+hipError_t launch_norm(int dtype, bool in_f32, bool layer_norm, const void* in, const void* g,
+                       const void* b, void* out, float* copy_f32, int rows, int H, float eps,
+                       hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (dtype == 0)
+    norm_dispatch<float, float>(layer_norm, in, g, b, out, copy_f32, rows, H, eps, s);
+  else if (in_f32)
+    norm_dispatch<float, bf16>(layer_norm, in, g, b, out, copy_f32, rows, H, eps, s);
+  else
+    norm_dispatch<bf16, bf16>(layer_norm, in, g, b, out, copy_f32, rows, H, eps, s);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ RoPE + KV append
+// Block: heads_per_block heads x (hd/2) threads; thread i rotates the pair
+// (i, i + hd/2) of q and k by angle pos * base^(-2i/hd) (angle in fp64), writes
+// q back in place and k, v to the cache at (slot, pos).
+template <typename T>
+__global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a, int heads_per_block) {
+  const int half = a.hd / 2;
+  const int h = blockIdx.y * heads_per_block + threadIdx.x / half;
+  const int i = threadIdx.x % half;
+  if (h >= a.nh) return;
+  const int row = blockIdx.x;
+  const int slot = a.row_slot[row];
+  const int pos = a.row_pos[row];
+  T* base = reinterpret_cast<T*>(a.qkv) + (size_t)row * (3 * a.nh * a.hd);
+  T* q = base + h * a.hd;
+  T* k = base + a.nh * a.hd + h * a.hd;
+  const T* v = base + 2 * a.nh * a.hd + h * a.hd;
+  float q0 = to_f<T>(q[i]), q1 = to_f<T>(q[i + half]);
+  float k0 = to_f<T>(k[i]), k1 = to_f<T>(k[i + half]);
+  if (a.rope) {
+    const double theta = pow((double)a.base, -2.0 * (double)i / (double)a.hd);
+    double sd, cd;
+    sincos((double)pos * theta, &sd, &cd);
+    const float c = (float)cd, sn = (float)sd;
+    const float nq0 = q0 * c - q1 * sn, nq1 = q0 * sn + q1 * c;
+    const float nk0 = k0 * c - k1 * sn, nk1 = k0 * sn + k1 * c;
+    q0 = nq0; q1 = nq1; k0 = nk0; k1 = nk1;
+    q[i] = from_f<T>(q0);
+    q[i + half] = from_f<T>(q1);
+  }
+  T* cache = reinterpret_cast<T*>(a.kv_layer);
+  T* kd = cache + (size_t)slot * a.st.slot + (size_t)h * a.st.head + (size_t)pos * a.st.pos;
+  T* vd = kd + a.st.kv;
+  kd[i] = from_f<T>(k0);
+  kd[i + half] = from_f<T>(k1);
+  vd[i] = v[i];
+  vd[i + half] = v[i + half];
+}
+
+hipError_t launch_rope_append(int dtype, const RopeArgs& a, hipStream_t s) {
+  if (a.T <= 0) return hipSuccess;
+  const int half = a.hd / 2;
+  const int hpb = 256 / half;
+  dim3 grid(a.T, (a.nh + hpb - 1) / hpb);
+  if (dtype == 0)
+    hipLaunchKernelGGL(rope_append_kernel<float>, grid, dim3(hpb * half), 0, s, a, hpb);
+  else
+    hipLaunchKernelGGL(rope_append_kernel<bf16>, grid, dim3(hpb * half), 0, s, a, hpb);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ casts
+template <typename T>
+__global__ void cast_kernel(const float* __restrict__ in, T* __restrict__ out, size_t n) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    out[i] = from_f<T>(in[i]);
+}
+
+hipError_t launch_cast_out(int dtype, const float* acc, void* out, size_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const int blocks = (int)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096);
+  if (dtype == 0)
+    hipLaunchKernelGGL(cast_kernel<float>, dim3(blocks), dim3(256), 0, s, acc, (float*)out, n);
+  else
+    hipLaunchKernelGGL(cast_kernel<bf16>, dim3(blocks), dim3(256), 0, s, acc, (bf16*)out, n);
+  return hipGetLastError();
+}
+
+template <typename T>
+__global__ void to_f32_kernel(const T* __restrict__ in, float* __restrict__ out, size_t n) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    out[i] = to_f<T>(in[i]);
+}
+
+hipError_t launch_to_f32(int dtype, const void* in, float* out, size_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const int blocks = (int)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096);
+  if (dtype == 0)
+    hipLaunchKernelGGL(to_f32_kernel<float>, dim3(blocks), dim3(256), 0, s, (const float*)in, out, n);
+  else
+    hipLaunchKernelGGL(to_f32_kernel<bf16>, dim3(blocks), dim3(256), 0, s, (const bf16*)in, out, n);
+  return hipGetLastError();
+}
+
+}  // namespace sarathi

@@ -1,0 +1,90 @@
+// Host-side launchers of the gfx950 kernels (implemented in the .hip files).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "common.h"
+
+namespace sarathi {
+
+// ---- batch metadata (int32 arrays in the workspace), written by a kernel
+// whose arguments carry the host values (stream-ordered, no staging buffer).
+constexpr int META_CHUNK = 640;
+struct MetaChunk {
+  int count;
+  int values[META_CHUNK];
+};
+hipError_t launch_meta_write(const MetaChunk& chunk, int* dst, hipStream_t s);
+
+// ---- norms (one row per block).  in: [rows, H] of Tin; out: [rows, H] of dtype.
+// copy_f32 (optional): receives the input as fp32 (residual-stream init).
+hipError_t launch_norm(int dtype, bool in_f32, bool layer_norm, const void* in, const void* g,
+                       const void* b, void* out, float* copy_f32, int rows, int H, float eps,
+                       hipStream_t s);
+
+// ---- rotary embedding of q, k in place of the preproj output and K/V append.
+struct RopeArgs {
+  void* qkv;            // [T, 3*nh*hd]
+  int T, nh, hd;
+  int rope;
+  float base;
+  const int* row_slot;  // [T]
+  const int* row_pos;   // [T]
+  void* kv_layer;       // base of this layer's cache
+  KVStrides st;
+};
+hipError_t launch_rope_append(int dtype, const RopeArgs& a, hipStream_t s);
+
+// ---- linear ops (see sarathi.h for the kinds).
+enum LinearKind { LIN_PLAIN = 0, LIN_RESID = 1, LIN_RESID_F32IN = 2, LIN_SWIGLU = 3, LIN_GELU = 4 };
+struct LinearArgs {
+  int kind;
+  int M, N, K;          // N = output columns
+  const void* x;        // [M, K]
+  const void* w;        // [N or 2N, K]
+  const void* resid;    // LIN_RESID: dtype [M,N]; LIN_RESID_F32IN: fp32 [M,N]
+  void* out;            // LIN_RESID: fp32 [M,N]; others dtype [M,N]
+  float* acc;           // LIN_RESID_F32IN: fp32 [M,N] split-K accumulator (null: no split-K)
+  bool allow_split;     // split-K permitted (LIN_RESID accumulates into out itself)
+  bool acc_ready;       // the accumulator already holds the residual as fp32
+};
+hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s);
+
+// ---- attention
+struct PrefillArgs {
+  const void* qkv;      // chunk rows 0..C-1, q columns rotated
+  int ld_qkv;
+  const void* kv_layer;
+  KVStrides st;
+  int slot, offset, C, nh, hd;
+  void* out;            // [T, nh*hd], chunk rows 0..C-1
+  int ld_out;
+};
+hipError_t launch_attn_prefill(int dtype, const PrefillArgs& a, hipStream_t s);
+
+// Row attention: each row r in [row_base, T) attends to keys 0..row_pos[r]
+// of slot row_slot[r], split into work items of split_keys keys.
+struct RowAttnArgs {
+  const void* qkv;
+  int ld_qkv;
+  const void* kv_layer;
+  KVStrides st;
+  const int* row_slot;
+  const int* row_pos;
+  const int* split0;    // [n_rows + 1] first work item of each row
+  const int* work;      // [n_work] (row_rel << 12) | split
+  int row_base, n_rows, n_work, split_keys, nh, hd;
+  float* part;          // [n_work, nh, hd + 2]
+  void* out;
+  int ld_out;
+};
+hipError_t launch_attn_rows(int dtype, const RowAttnArgs& a, hipStream_t s);
+
+// fp32 accumulator -> dtype
+hipError_t launch_cast_out(int dtype, const float* acc, void* out, size_t n, hipStream_t s);
+// dtype (or fp32 when dtype == 0) -> fp32 copy
+hipError_t launch_to_f32(int dtype, const void* in, float* out, size_t n, hipStream_t s);
+
+}  // namespace sarathi

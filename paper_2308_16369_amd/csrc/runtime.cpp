@@ -1,0 +1,524 @@
+// Host runtime of libsarathi: argument validation (entirely on the host,
+// before anything is enqueued), workspace layout, batch metadata upload and
+// the launch sequence of one decoder layer over a decode-maximal hybrid batch
+// (Sec. 4.3: one matmul per linear op over all rows; chunk attention and
+// decode attention separately).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "sarathi.h"
+
+using namespace sarathi;
+
+struct sarathi_kv {
+  sarathi_model_cfg cfg;
+  int n_slots;
+  int max_seq_len;
+  void* mem;
+  size_t bytes;
+  KVStrides st;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(SARATHI_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr int SPLIT_KEYS = 256;   // keys per row-attention work item
+
+size_t esize(const sarathi_model_cfg* c) { return c->dtype == SARATHI_BF16 ? 2 : 4; }
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+int check_cfg(const sarathi_model_cfg* c) {
+  if (!c) return fail(SARATHI_EINVAL, "cfg is NULL");
+  if (c->dtype != SARATHI_F32 && c->dtype != SARATHI_BF16)
+    return fail(SARATHI_EUNSUPPORTED, "dtype %d not supported (F32 or BF16)", c->dtype);
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(SARATHI_EUNSUPPORTED, "head_dim %d not supported (64 or 128)", c->head_dim);
+  if (c->hidden <= 0 || c->hidden % 8) return fail(SARATHI_EUNSUPPORTED, "hidden %d must be a positive multiple of 8", c->hidden);
+  if (c->ffn <= 0 || c->ffn % 8) return fail(SARATHI_EUNSUPPORTED, "ffn %d must be a positive multiple of 8", c->ffn);
+  if (c->n_heads <= 0 || c->n_heads > 65535) return fail(SARATHI_EUNSUPPORTED, "n_heads %d out of range", c->n_heads);
+  if (c->n_layers <= 0) return fail(SARATHI_EINVAL, "n_layers %d must be positive", c->n_layers);
+  if (c->norm != SARATHI_NORM_RMS && c->norm != SARATHI_NORM_LAYER) return fail(SARATHI_EUNSUPPORTED, "norm %d", c->norm);
+  if (c->act != SARATHI_ACT_SWIGLU && c->act != SARATHI_ACT_GELU) return fail(SARATHI_EUNSUPPORTED, "act %d", c->act);
+  if (c->rope != 0 && c->rope != 1) return fail(SARATHI_EINVAL, "rope must be 0 or 1");
+  if (c->rope && !(c->rope_base > 1.0f)) return fail(SARATHI_EINVAL, "rope_base must be > 1");
+  if (!(c->eps > 0.0f)) return fail(SARATHI_EINVAL, "eps must be > 0");
+  return SARATHI_OK;
+}
+
+bool same_cfg(const sarathi_model_cfg* a, const sarathi_model_cfg* b) {
+  return a->hidden == b->hidden && a->n_heads == b->n_heads && a->head_dim == b->head_dim && a->ffn == b->ffn &&
+         a->n_layers == b->n_layers && a->norm == b->norm && a->act == b->act && a->rope == b->rope &&
+         a->rope_base == b->rope_base && a->eps == b->eps && a->dtype == b->dtype;
+}
+
+struct Layout {
+  size_t a, qkv, o, hres, m, yacc, part, meta, ping0, ping1, total;
+  int max_work;
+};
+
+Layout make_layout(const sarathi_model_cfg* c, int T, int S) {
+  Layout L{};
+  const size_t es = esize(c);
+  const size_t H = c->hidden, F = c->ffn, QD = (size_t)c->n_heads * c->head_dim;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { const size_t at = off; off = align256(off + bytes); return at; };
+  L.a = take(T * H * es);
+  L.qkv = take(T * 3 * QD * es);
+  L.o = take(T * QD * es);
+  L.hres = take(T * H * 4);
+  L.m = take(T * F * es);
+  L.yacc = take(T * H * 4);
+  L.max_work = T * ((S + SPLIT_KEYS - 1) / SPLIT_KEYS);
+  L.part = take((size_t)L.max_work * c->n_heads * (c->head_dim + 2) * 4);
+  L.meta = take(((size_t)T * 3 + 1 + L.max_work) * 4);
+  L.ping0 = take(T * H * es);
+  L.ping1 = take(T * H * es);
+  L.total = off;
+  return L;
+}
+
+// Host-side description of the batch and its device metadata.
+struct Plan {
+  int C, B, T, row_base, n_rows, n_work;
+  std::vector<int> meta;          // row_slot[T] row_pos[T] split0[n_rows+1] work[n_work]
+  size_t o_slot, o_pos, o_split0, o_work;   // int offsets into meta
+};
+
+int check_batch(const sarathi_model_cfg* cfg, const sarathi_kv* kv, const sarathi_hybrid_batch* b) {
+  if (!b) return fail(SARATHI_EINVAL, "batch is NULL");
+  const int C = b->chunk_len, B = b->n_decodes, S = kv->max_seq_len;
+  if (C < 0) return fail(SARATHI_ERANGE, "chunk_len %d < 0", C);
+  if (B < 0) return fail(SARATHI_EINVAL, "n_decodes %d < 0", B);
+  if (C + B == 0) return fail(SARATHI_EINVAL, "empty batch (chunk_len + n_decodes == 0)");
+  if (C + B > (1 << 19)) return fail(SARATHI_EINVAL, "batch of %d rows too large", C + B);
+  std::vector<char> used(kv->n_slots, 0);
+  if (C > 0) {
+    if (b->prefill_slot < 0 || b->prefill_slot >= kv->n_slots)
+      return fail(SARATHI_EINVAL, "prefill_slot %d outside [0, %d)", b->prefill_slot, kv->n_slots);
+    if (b->chunk_offset < 0) return fail(SARATHI_ERANGE, "chunk_offset %d < 0", b->chunk_offset);
+    if ((long)b->chunk_offset + C > S)
+      return fail(SARATHI_ERANGE, "chunk_offset %d + chunk_len %d > max_seq_len %d", b->chunk_offset, C, S);
+    used[b->prefill_slot] = 1;
+  }
+  if (B > 0) {
+    if (!b->decode_slots || !b->decode_ctx_lens) return fail(SARATHI_EINVAL, "decode arrays are NULL");
+    for (int i = 0; i < B; ++i) {
+      const int s = b->decode_slots[i], ctx = b->decode_ctx_lens[i];
+      if (s < 0 || s >= kv->n_slots) return fail(SARATHI_EINVAL, "decode_slots[%d] = %d outside [0, %d)", i, s, kv->n_slots);
+      if (used[s]) return fail(SARATHI_EINVAL, "slot %d appears twice in the batch", s);
+      used[s] = 1;
+      if (ctx < 0) return fail(SARATHI_ERANGE, "decode_ctx_lens[%d] = %d < 0", i, ctx);
+      if ((long)ctx + 1 > S) return fail(SARATHI_ERANGE, "decode_ctx_lens[%d] + 1 = %d > max_seq_len %d", i, ctx + 1, S);
+    }
+  }
+  (void)cfg;
+  return SARATHI_OK;
+}
+
+Plan make_plan(const sarathi_model_cfg* cfg, const sarathi_hybrid_batch* b) {
+  Plan p;
+  p.C = b->chunk_len;
+  p.B = b->n_decodes;
+  p.T = p.C + p.B;
+  // bf16: the chunk goes to the MFMA prefill kernel, the decodes to row
+  // attention.  fp32: every row goes to row attention (a chunk row at
+  // position p is attention over keys 0..p, like a decode with ctx = p).
+  p.row_base = (cfg->dtype == SARATHI_BF16) ? p.C : 0;
+  p.n_rows = p.T - p.row_base;
+  std::vector<int> slot(p.T), pos(p.T);
+  for (int r = 0; r < p.C; ++r) { slot[r] = b->prefill_slot; pos[r] = b->chunk_offset + r; }
+  for (int i = 0; i < p.B; ++i) { slot[p.C + i] = b->decode_slots[i]; pos[p.C + i] = b->decode_ctx_lens[i]; }
+  std::vector<int> split0(p.n_rows + 1), work;
+  for (int r = 0; r < p.n_rows; ++r) {
+    split0[r] = (int)work.size();
+    const int nk = pos[p.row_base + r] + 1;
+    const int ns = (nk + SPLIT_KEYS - 1) / SPLIT_KEYS;
+    for (int s = 0; s < ns; ++s) work.push_back((r << 12) | s);
+  }
+  split0[p.n_rows] = (int)work.size();
+  p.n_work = (int)work.size();
+  p.meta.reserve(3 * p.T + 1 + work.size());
+  p.o_slot = 0; p.meta.insert(p.meta.end(), slot.begin(), slot.end());
+  p.o_pos = p.meta.size(); p.meta.insert(p.meta.end(), pos.begin(), pos.end());
+  p.o_split0 = p.meta.size(); p.meta.insert(p.meta.end(), split0.begin(), split0.end());
+  p.o_work = p.meta.size(); p.meta.insert(p.meta.end(), work.begin(), work.end());
+  return p;
+}
+
+int check_weights(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, int layer) {
+  if (!w) return fail(SARATHI_EINVAL, "weights are NULL");
+  const void* need[] = {w->norm1_g, w->w_qkv, w->w_o, w->norm2_g, w->w_up, w->w_down};
+  for (const void* p : need)
+    if (!p) return fail(SARATHI_EINVAL, "layer %d: a weight pointer is NULL", layer);
+  if (cfg->norm == SARATHI_NORM_LAYER && (!w->norm1_b || !w->norm2_b))
+    return fail(SARATHI_EINVAL, "layer %d: LayerNorm biases are NULL", layer);
+  for (const void* p : {w->w_qkv, w->w_o, w->w_up, w->w_down})
+    if (!aligned16(p)) return fail(SARATHI_EINVAL, "layer %d: weight matrices must be 16-byte aligned", layer);
+  return SARATHI_OK;
+}
+
+// ---- stage timing: a pool of HIP events recorded at stage boundaries.
+constexpr int EV_PER_CALL = SARATHI_N_STAGES + 1;
+struct Profiler {
+  std::mutex mu;
+  bool on = false;
+  int max_calls = 0;
+  int calls = 0;
+  std::vector<hipEvent_t> pool;
+};
+Profiler g_prof;
+
+// Events of the next layer call (nullptr when not recording).
+hipEvent_t* prof_claim() {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  if (!g_prof.on || g_prof.calls >= g_prof.max_calls) return nullptr;
+  return g_prof.pool.data() + EV_PER_CALL * (g_prof.calls++);
+}
+
+struct Ctx {
+  const sarathi_model_cfg* cfg;
+  sarathi_kv* kv;
+  const Plan* plan;
+  Layout L;
+  char* ws;
+  hipStream_t s;
+};
+
+int upload_meta(const Ctx& c) {
+  int* dst = reinterpret_cast<int*>(c.ws + c.L.meta);
+  const std::vector<int>& m = c.plan->meta;
+  for (size_t at = 0; at < m.size(); at += META_CHUNK) {
+    MetaChunk chunk;
+    chunk.count = (int)std::min<size_t>(META_CHUNK, m.size() - at);
+    std::memcpy(chunk.values, m.data() + at, chunk.count * sizeof(int));
+    hipError_t e = launch_meta_write(chunk, dst + at, c.s);
+    if (e != hipSuccess) return hip_fail(e, "metadata upload");
+  }
+  return SARATHI_OK;
+}
+
+// One decoder layer; metadata already on the device.
+int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const void* x_in, void* x_out) {
+  const sarathi_model_cfg* cfg = c.cfg;
+  const Plan& P = *c.plan;
+  const int T = P.T, H = cfg->hidden, nh = cfg->n_heads, hd = cfg->head_dim, F = cfg->ffn;
+  const int QD = nh * hd;
+  const int dt = cfg->dtype;
+  const bool ln = cfg->norm == SARATHI_NORM_LAYER;
+  char* ws = c.ws;
+  const int* meta = reinterpret_cast<const int*>(ws + c.L.meta);
+  float* hres = reinterpret_cast<float*>(ws + c.L.hres);
+  float* yacc = reinterpret_cast<float*>(ws + c.L.yacc);
+  char* kv_layer = static_cast<char*>(c.kv->mem) + (size_t)layer * c.kv->st.layer * esize(cfg);
+  hipError_t e;
+  hipEvent_t* ev = prof_claim();
+  int stage = 0;
+  auto mark = [&]() -> hipError_t { return ev ? hipEventRecord(ev[stage++], c.s) : hipSuccess; };
+#define SARATHI_MARK()                                          \
+  do {                                                          \
+    hipError_t me = mark();                                     \
+    if (me != hipSuccess) return hip_fail(me, "stage event");   \
+  } while (0)
+
+  // norm_1 (also leaves x in fp32 in hres, the split-K accumulator of postproj)
+  SARATHI_MARK();
+  e = launch_norm(dt, false, ln, x_in, w->norm1_g, w->norm1_b, ws + c.L.a, hres, T, H, cfg->eps, c.s);
+  if (e != hipSuccess) return hip_fail(e, "norm_1");
+
+  // preproj over all rows
+  SARATHI_MARK();
+  LinearArgs q{};
+  q.kind = LIN_PLAIN; q.M = T; q.N = 3 * QD; q.K = H; q.x = ws + c.L.a; q.w = w->w_qkv; q.out = ws + c.L.qkv;
+  e = launch_linear(dt, q, c.s);
+  if (e != hipSuccess) return hip_fail(e, "preproj");
+
+  // rotary embedding + in-place KV append
+  SARATHI_MARK();
+  RopeArgs ra{};
+  ra.qkv = ws + c.L.qkv; ra.T = T; ra.nh = nh; ra.hd = hd; ra.rope = cfg->rope; ra.base = cfg->rope_base;
+  ra.row_slot = meta + P.o_slot; ra.row_pos = meta + P.o_pos; ra.kv_layer = kv_layer; ra.st = c.kv->st;
+  e = launch_rope_append(dt, ra, c.s);
+  if (e != hipSuccess) return hip_fail(e, "rope/kv append");
+
+  // attention: the chunk and the decodes separately
+  SARATHI_MARK();
+  if (dt == SARATHI_BF16 && P.C > 0) {
+    PrefillArgs pa{};
+    pa.qkv = ws + c.L.qkv; pa.ld_qkv = 3 * QD; pa.kv_layer = kv_layer; pa.st = c.kv->st;
+    pa.slot = c.plan->meta[P.o_slot]; pa.offset = c.plan->meta[P.o_pos]; pa.C = P.C; pa.nh = nh; pa.hd = hd;
+    pa.out = ws + c.L.o; pa.ld_out = QD;
+    e = launch_attn_prefill(dt, pa, c.s);
+    if (e != hipSuccess) return hip_fail(e, "prefill attention");
+  }
+  SARATHI_MARK();
+  if (P.n_rows > 0) {
+    RowAttnArgs da{};
+    da.qkv = ws + c.L.qkv; da.ld_qkv = 3 * QD; da.kv_layer = kv_layer; da.st = c.kv->st;
+    da.row_slot = meta + P.o_slot; da.row_pos = meta + P.o_pos; da.split0 = meta + P.o_split0;
+    da.work = meta + P.o_work; da.row_base = P.row_base; da.n_rows = P.n_rows; da.n_work = P.n_work;
+    da.split_keys = SPLIT_KEYS; da.nh = nh; da.hd = hd;
+    da.part = reinterpret_cast<float*>(ws + c.L.part); da.out = ws + c.L.o; da.ld_out = QD;
+    e = launch_attn_rows(dt, da, c.s);
+    if (e != hipSuccess) return hip_fail(e, "decode attention");
+  }
+
+  // postproj + residual -> hres (fp32)
+  SARATHI_MARK();
+  LinearArgs po{};
+  po.kind = LIN_RESID; po.M = T; po.N = H; po.K = QD; po.x = ws + c.L.o; po.w = w->w_o; po.resid = x_in;
+  po.out = hres; po.allow_split = true; po.acc_ready = true;
+  e = launch_linear(dt, po, c.s);
+  if (e != hipSuccess) return hip_fail(e, "postproj");
+
+  // norm_2 (also copies hres into yacc, the split-K accumulator of ffn_ln2)
+  SARATHI_MARK();
+  e = launch_norm(dt, true, ln, hres, w->norm2_g, w->norm2_b, ws + c.L.a, yacc, T, H, cfg->eps, c.s);
+  if (e != hipSuccess) return hip_fail(e, "norm_2");
+
+  // ffn_ln1 + activation
+  SARATHI_MARK();
+  LinearArgs up{};
+  up.kind = cfg->act == SARATHI_ACT_SWIGLU ? LIN_SWIGLU : LIN_GELU;
+  up.M = T; up.N = F; up.K = H; up.x = ws + c.L.a; up.w = w->w_up; up.out = ws + c.L.m;
+  e = launch_linear(dt, up, c.s);
+  if (e != hipSuccess) return hip_fail(e, "ffn_ln1");
+
+  // ffn_ln2 + residual -> x_out
+  SARATHI_MARK();
+  LinearArgs dn{};
+  dn.kind = LIN_RESID_F32IN; dn.M = T; dn.N = H; dn.K = F; dn.x = ws + c.L.m; dn.w = w->w_down; dn.resid = hres;
+  dn.out = x_out; dn.acc = yacc; dn.allow_split = true; dn.acc_ready = true;
+  e = launch_linear(dt, dn, c.s);
+  if (e != hipSuccess) return hip_fail(e, "ffn_ln2");
+  SARATHI_MARK();
+#undef SARATHI_MARK
+  return SARATHI_OK;
+}
+
+int prepare(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, int n_w, sarathi_kv* kv,
+            const sarathi_hybrid_batch* batch, const void* x_in, void* x_out, void* ws, size_t ws_bytes,
+            Plan* plan, Layout* L) {
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (!kv) return fail(SARATHI_EINVAL, "kv is NULL");
+  if (!same_cfg(cfg, &kv->cfg)) return fail(SARATHI_EINVAL, "cfg differs from the cfg the KV cache was bound with");
+  rc = check_batch(cfg, kv, batch);
+  if (rc) return rc;
+  for (int i = 0; i < n_w; ++i) {
+    rc = check_weights(cfg, w + i, i);
+    if (rc) return rc;
+  }
+  if (!x_in || !x_out) return fail(SARATHI_EINVAL, "x_in / x_out is NULL");
+  if (!ws) return fail(SARATHI_EINVAL, "workspace is NULL");
+  if (x_in == x_out) return fail(SARATHI_EINVAL, "x_in and x_out alias");
+  if (!aligned16(x_in) || !aligned16(x_out) || !aligned16(ws))
+    return fail(SARATHI_EINVAL, "x_in, x_out and ws must be 16-byte aligned");
+  const int T = batch->chunk_len + batch->n_decodes;
+  *L = make_layout(cfg, T, kv->max_seq_len);
+  if (ws_bytes < L->total)
+    return fail(SARATHI_ENOSPC, "workspace of %zu bytes < %zu needed", ws_bytes, L->total);
+  const char* wb = static_cast<const char*>(ws);
+  const char* xi = static_cast<const char*>(x_in);
+  const char* xo = static_cast<const char*>(x_out);
+  const size_t xbytes = (size_t)T * cfg->hidden * esize(cfg);
+  auto overlap = [](const char* a, size_t na, const char* b, size_t nb) { return a < b + nb && b < a + na; };
+  if (overlap(xi, xbytes, wb, L->total) || overlap(xo, xbytes, wb, L->total) || overlap(xi, xbytes, xo, xbytes))
+    return fail(SARATHI_EINVAL, "x_in, x_out and the workspace must not overlap");
+  *plan = make_plan(cfg, batch);
+  return SARATHI_OK;
+}
+
+}  // namespace
+
+// ============================================================================ C-ABI
+
+extern "C" {
+
+int sarathi_version(void) { return 1; }
+
+const char* sarathi_last_error(void) { return g_err.c_str(); }
+
+size_t sarathi_kv_bytes(const sarathi_model_cfg* cfg, int n_slots, int max_seq_len) {
+  if (check_cfg(cfg) != SARATHI_OK || n_slots < 1 || max_seq_len < 1) return 0;
+  return (size_t)cfg->n_layers * n_slots * 2 * cfg->n_heads * (size_t)max_seq_len * cfg->head_dim * esize(cfg);
+}
+
+int sarathi_kv_alloc(const sarathi_model_cfg* cfg, int n_slots, int max_seq_len, void* dev_mem, size_t dev_bytes,
+                     sarathi_kv** out) {
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (!out) return fail(SARATHI_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (!dev_mem) return fail(SARATHI_EINVAL, "dev_mem is NULL");
+  if (!aligned16(dev_mem)) return fail(SARATHI_EINVAL, "dev_mem must be 16-byte aligned");
+  if (n_slots < 1 || n_slots > (1 << 20)) return fail(SARATHI_EINVAL, "n_slots %d out of range", n_slots);
+  if (max_seq_len < 1 || max_seq_len > (1 << 20)) return fail(SARATHI_EINVAL, "max_seq_len %d out of range", max_seq_len);
+  const size_t need = sarathi_kv_bytes(cfg, n_slots, max_seq_len);
+  if (dev_bytes < need) return fail(SARATHI_ENOSPC, "KV memory of %zu bytes < %zu needed", dev_bytes, need);
+  sarathi_kv* kv = new sarathi_kv;
+  kv->cfg = *cfg;
+  kv->n_slots = n_slots;
+  kv->max_seq_len = max_seq_len;
+  kv->mem = dev_mem;
+  kv->bytes = dev_bytes;
+  kv->st.pos = cfg->head_dim;
+  kv->st.head = (size_t)max_seq_len * cfg->head_dim;
+  kv->st.kv = kv->st.head * cfg->n_heads;
+  kv->st.slot = kv->st.kv * 2;
+  kv->st.layer = kv->st.slot * n_slots;
+  *out = kv;
+  return SARATHI_OK;
+}
+
+void sarathi_kv_free(sarathi_kv* kv) { delete kv; }
+
+int sarathi_kv_get_strides(const sarathi_kv* kv, sarathi_kv_strides* out) {
+  if (!kv || !out) return fail(SARATHI_EINVAL, "NULL argument");
+  out->layer = kv->st.layer; out->slot = kv->st.slot; out->kv = kv->st.kv; out->head = kv->st.head; out->pos = kv->st.pos;
+  return SARATHI_OK;
+}
+
+size_t sarathi_workspace_bytes(const sarathi_model_cfg* cfg, int max_tokens, int max_decodes, int max_seq_len) {
+  if (check_cfg(cfg) != SARATHI_OK || max_tokens < 1 || max_decodes < 0 || max_seq_len < 1) return 0;
+  (void)max_decodes;
+  return make_layout(cfg, max_tokens, max_seq_len).total;
+}
+
+int sarathi_workspace_layout(const sarathi_model_cfg* cfg, int n_tokens, int n_decodes, int max_seq_len,
+                             sarathi_ws_layout* out) {
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (!out) return fail(SARATHI_EINVAL, "out is NULL");
+  if (n_tokens < 1 || n_decodes < 0 || n_decodes > n_tokens || max_seq_len < 1)
+    return fail(SARATHI_EINVAL, "bad sizes");
+  const Layout L = make_layout(cfg, n_tokens, max_seq_len);
+  out->a = L.a; out->qkv = L.qkv; out->o = L.o; out->hres = L.hres; out->m = L.m; out->total = L.total;
+  return SARATHI_OK;
+}
+
+int sarathi_hybrid_layer_forward(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, sarathi_kv* kv,
+                                 int layer, const sarathi_hybrid_batch* batch, const void* x_in, void* x_out,
+                                 void* ws, size_t ws_bytes, void* hip_stream) {
+  Plan plan;
+  Layout L;
+  int rc = prepare(cfg, w, 1, kv, batch, x_in, x_out, ws, ws_bytes, &plan, &L);
+  if (rc) return rc;
+  if (layer < 0 || layer >= cfg->n_layers) return fail(SARATHI_EINVAL, "layer %d outside [0, %d)", layer, cfg->n_layers);
+  Ctx c{cfg, kv, &plan, L, static_cast<char*>(ws), static_cast<hipStream_t>(hip_stream)};
+  rc = upload_meta(c);
+  if (rc) return rc;
+  return layer_body(c, w, layer, x_in, x_out);
+}
+
+int sarathi_model_step(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, sarathi_kv* kv,
+                       const sarathi_hybrid_batch* batch, const void* x_in, void* x_out, void* ws,
+                       size_t ws_bytes, void* hip_stream) {
+  if (!cfg) return fail(SARATHI_EINVAL, "cfg is NULL");
+  Plan plan;
+  Layout L;
+  int rc = prepare(cfg, w, cfg->n_layers > 0 ? cfg->n_layers : 0, kv, batch, x_in, x_out, ws, ws_bytes, &plan, &L);
+  if (rc) return rc;
+  Ctx c{cfg, kv, &plan, L, static_cast<char*>(ws), static_cast<hipStream_t>(hip_stream)};
+  rc = upload_meta(c);
+  if (rc) return rc;
+  char* ping[2] = {c.ws + L.ping0, c.ws + L.ping1};
+  const int n = cfg->n_layers;
+  for (int l = 0; l < n; ++l) {
+    const void* in = (l == 0) ? x_in : ping[l & 1];
+    void* out = (l == n - 1) ? x_out : ping[(l + 1) & 1];
+    rc = layer_body(c, w + l, l, in, out);
+    if (rc) return rc;
+  }
+  return SARATHI_OK;
+}
+
+int sarathi_profile_begin(int max_calls) {
+  if (max_calls < 1 || max_calls > (1 << 16)) return fail(SARATHI_EINVAL, "max_calls %d out of range", max_calls);
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  const size_t need = (size_t)EV_PER_CALL * max_calls;
+  while (g_prof.pool.size() < need) {
+    hipEvent_t e;
+    hipError_t he = hipEventCreate(&e);
+    if (he != hipSuccess) return hip_fail(he, "hipEventCreate");
+    g_prof.pool.push_back(e);
+  }
+  g_prof.on = true;
+  g_prof.max_calls = max_calls;
+  g_prof.calls = 0;
+  return SARATHI_OK;
+}
+
+int sarathi_profile_end(double* stage_ms, int* n_calls) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  if (!g_prof.on) return fail(SARATHI_EINVAL, "profiling was not started");
+  if (!stage_ms || !n_calls) return fail(SARATHI_EINVAL, "NULL output");
+  g_prof.on = false;
+  for (int s = 0; s < SARATHI_N_STAGES; ++s) stage_ms[s] = 0.0;
+  *n_calls = g_prof.calls;
+  if (g_prof.calls == 0) return SARATHI_OK;
+  hipError_t he = hipEventSynchronize(g_prof.pool[(size_t)EV_PER_CALL * g_prof.calls - 1]);
+  if (he != hipSuccess) return hip_fail(he, "hipEventSynchronize");
+  for (int c = 0; c < g_prof.calls; ++c) {
+    hipEvent_t* ev = g_prof.pool.data() + (size_t)EV_PER_CALL * c;
+    for (int s = 0; s < SARATHI_N_STAGES; ++s) {
+      float ms = 0.f;
+      he = hipEventElapsedTime(&ms, ev[s], ev[s + 1]);
+      if (he != hipSuccess) return hip_fail(he, "hipEventElapsedTime");
+      stage_ms[s] += ms;
+    }
+  }
+  return SARATHI_OK;
+}
+
+size_t sarathi_linear_scratch_bytes(int M, int N) {
+  if (M < 1 || N < 1) return 0;
+  return (size_t)M * N * 4;
+}
+
+int sarathi_linear(int dtype, int kind, int M, int N, int K, const void* x, const void* w, const void* resid,
+                   void* out, void* scratch, size_t scratch_bytes, void* hip_stream) {
+  if (dtype != SARATHI_F32 && dtype != SARATHI_BF16) return fail(SARATHI_EUNSUPPORTED, "dtype %d", dtype);
+  if (kind < SARATHI_LINEAR_PLAIN || kind > SARATHI_LINEAR_GELU) return fail(SARATHI_EINVAL, "kind %d", kind);
+  if (M < 1 || N < 1 || K < 1) return fail(SARATHI_EINVAL, "M, N, K must be positive");
+  if (K % 8) return fail(SARATHI_EUNSUPPORTED, "K %d must be a multiple of 8", K);
+  if (!x || !w || !out) return fail(SARATHI_EINVAL, "NULL pointer");
+  const bool needs_resid = kind == SARATHI_LINEAR_RESID || kind == SARATHI_LINEAR_RESID_F32IN;
+  if (needs_resid && !resid) return fail(SARATHI_EINVAL, "resid is NULL");
+  if (!aligned16(x) || !aligned16(w)) return fail(SARATHI_EINVAL, "x and w must be 16-byte aligned");
+  LinearArgs a{};
+  a.kind = kind; a.M = M; a.N = N; a.K = K; a.x = x; a.w = w; a.resid = resid; a.out = out;
+  a.allow_split = kind == SARATHI_LINEAR_RESID ||
+                  (kind == SARATHI_LINEAR_RESID_F32IN && scratch && scratch_bytes >= sarathi_linear_scratch_bytes(M, N));
+  a.acc = (kind == SARATHI_LINEAR_RESID_F32IN && a.allow_split) ? static_cast<float*>(scratch) : nullptr;
+  a.acc_ready = false;
+  hipError_t e = launch_linear(dtype, a, static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail(e, "linear");
+  return SARATHI_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,239 @@
+"""GPU parity: the HIP library (through its C-ABI) against the float64 oracle.
+
+Tolerances (per tensor, max |gpu - oracle| / max |oracle|): 2e-2 for bf16
+runs, 1e-4 for fp32 runs.  KV indexing is checked bit-exactly: exactly the
+oracle's (layer, slot, position) entries change, every other element keeps
+its bit pattern (including the NaN sentinel of empty positions, so an
+over-read would also poison the outputs)."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+from gpu_harness import (TOL, DeviceModel, assert_checks, bits_of, compare_layer, delta_err, from_dev,  # noqa: E402
+                         log, oracle_batch, rel_err, to_dev)
+from paper_2308_16369_amd import sarathi as S  # noqa: E402
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    # On a GPU machine the library must be there: no fallback exists.
+    S.lib()
+
+
+def run_and_check(inst: wl.HostInstance, label: str, layer: int = 0):
+    log(f"{label}: T={inst.batch.n_tokens} C={inst.batch.chunk_len}@{inst.batch.chunk_offset} "
+        f"B={inst.batch.n_decodes} dtype={inst.shape.dtype}")
+    dm = DeviceModel(inst)
+    x = to_dev(inst.x, inst.shape.dtype)
+    before = bits_of(dm.kv_dev)
+    y = dm.layer(layer, inst.batch, x)
+    torch.cuda.synchronize()
+    ref = oracle.layer_forward(inst.shape, inst.weights[layer], inst.kv[layer].copy(), oracle_batch(inst.batch),
+                               inst.x)
+    checks = compare_layer(dm, layer, inst.batch, inst.x.astype(np.float64), y, before, inst.kv[layer], ref)
+    assert_checks(checks, label)
+    assert np.all(np.isfinite(from_dev(y)))
+
+
+# ============================================================================ linear ops
+
+LIN_SHAPES = [(72, 200, 264), (320, 640, 512), (283, 1000, 1032), (5, 17, 8), (544, 384, 256), (160, 128, 64)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("kind", [S.LINEAR_PLAIN, S.LINEAR_RESID, S.LINEAR_RESID_F32IN, S.LINEAR_SWIGLU,
+                                  S.LINEAR_GELU])
+@pytest.mark.parametrize("mnk", LIN_SHAPES)
+def test_linear_matches_oracle(dtype, kind, mnk):
+    M, N, K = mnk
+    rng = np.random.default_rng(M * 7 + N * 3 + K + kind)
+    st = (lambda a: wl.round_to_bf16(a)) if dtype == "bf16" else (lambda a: a.astype(np.float32))
+    x = st(rng.standard_normal((M, K)).astype(np.float32))
+    wrows = 2 * N if kind == S.LINEAR_SWIGLU else N
+    w = st((rng.standard_normal((wrows, K)) * 0.05).astype(np.float32))
+    resid = rng.standard_normal((M, N)).astype(np.float32)
+    if kind == S.LINEAR_RESID:
+        resid = st(resid)
+    z = oracle.linear(x, w)
+    if kind == S.LINEAR_PLAIN:
+        ref = z
+    elif kind in (S.LINEAR_RESID, S.LINEAR_RESID_F32IN):
+        ref = resid.astype(np.float64) + z
+    elif kind == S.LINEAR_SWIGLU:
+        ref = oracle.silu(z[:, :N]) * z[:, N:]
+    else:
+        ref = oracle.gelu(z)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    xd, wd = to_dev(x, dtype), to_dev(w, dtype)
+    rd = to_dev(resid, dtype) if kind == S.LINEAR_RESID else torch.from_numpy(resid).cuda()
+    out = torch.empty((M, N), dtype=torch.float32 if kind == S.LINEAR_RESID else tdt, device="cuda")
+    scratch = torch.empty(S.sarathi_linear_scratch_bytes(M, N), dtype=torch.uint8, device="cuda")
+    S.sarathi_linear(S.BF16 if dtype == "bf16" else S.F32, kind, M, N, K, xd.data_ptr(), wd.data_ptr(),
+                     rd.data_ptr() if kind in (S.LINEAR_RESID, S.LINEAR_RESID_F32IN) else 0, out.data_ptr(),
+                     scratch.data_ptr(), scratch.numel(), torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    got = from_dev(out)
+    err = rel_err(got, ref)
+    if kind in (S.LINEAR_RESID, S.LINEAR_RESID_F32IN):
+        out_dt = "f32" if kind == S.LINEAR_RESID else dtype
+        err = max(err, delta_err(got, ref, z, out_dt))
+    log(f"linear {dtype} kind {kind} {mnk}: err {err:.3e}")
+    assert err <= TOL[dtype]
+
+
+# ============================================================================ whole layer
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_layer_tiny_workload(dtype):
+    w = wl.TINY if dtype == "f32" else wl.with_dtype(wl.TINY, "bf16")
+    run_and_check(wl.generate(w), f"tiny layer {dtype}")
+
+
+def _tiny_shape(dtype, **kw):
+    return dataclasses.replace(wl.TINY.shape, dtype=dtype, **kw)
+
+
+EDGE = {
+    # name: (prefill_slot, offset, C, decode_slots, decode_ctx, S, n_slots)
+    "decode_only": (-1, 0, 0, [3, 0, 7, 5, 1, 2, 8, 6], [32, 77, 128, 0, 5, 250, 64, 100], 256, 9),
+    "prefill_only": (4, 128, 64, [], [], 256, 9),
+    "prefill_from_zero": (2, 0, 64, [0, 5, 8], [10, 1, 63], 256, 9),
+    "ragged_chunk": (6, 100, 37, [1, 2, 3, 4, 5], [7, 99, 128, 200, 33], 256, 9),
+    "single_token_chunk": (0, 200, 1, [1, 2], [31, 64], 256, 9),
+    "full_cache": (1, 192, 64, [0, 2, 3], [255, 254, 0], 256, 9),
+    "multi_split_decodes": (3, 700, 200, list(range(4, 20)),
+                            [256, 257, 511, 512, 513, 1000, 1087, 300, 640, 768, 900, 1023, 1024, 1050, 600, 700],
+                            1088, 20),
+    "many_decodes_bf16_tail": (-1, 0, 0, list(range(1, 70)), [(37 * i) % 300 for i in range(1, 70)], 320, 71),
+}
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("case", list(EDGE))
+def test_layer_edge_cases(dtype, case):
+    ps, off, C, ds, dc, S_, ns = EDGE[case]
+    b = wl.Batch(prefill_slot=ps, chunk_offset=off, chunk_len=C, decode_slots=np.array(ds, np.int32),
+                 decode_ctx=np.array(dc, np.int32))
+    inst = wl.make_instance(_tiny_shape(dtype), b, max_seq_len=S_, n_slots=ns, seed=11)
+    run_and_check(inst, f"edge {case} {dtype}")
+
+
+def test_layer_gpt_style_tiny_bf16():
+    shape = _tiny_shape("bf16", norm="layer", act="gelu", rope=False, eps=1e-5)
+    b = wl.Batch(prefill_slot=0, chunk_offset=64, chunk_len=100, decode_slots=np.array([1, 2, 3], np.int32),
+                 decode_ctx=np.array([5, 150, 255], np.int32))
+    run_and_check(wl.make_instance(shape, b, max_seq_len=256, n_slots=4, seed=3), "gpt-style tiny bf16")
+
+
+def test_layer_head_dim_128_tiny_bf16():
+    shape = _tiny_shape("bf16", hidden=512, n_heads=4, head_dim=128, ffn=1376)
+    b = wl.Batch(prefill_slot=2, chunk_offset=300, chunk_len=130, decode_slots=np.array([0, 1, 3], np.int32),
+                 decode_ctx=np.array([0, 511, 258], np.int32))
+    run_and_check(wl.make_instance(shape, b, max_seq_len=512, n_slots=4, seed=5), "hd128 tiny bf16")
+
+
+# ============================================================================ method invariants on the GPU
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_chunked_prefill_on_gpu_matches_one_shot_oracle(dtype):
+    """Chunks of a prompt through the library (KV grown in place between
+    calls) against the oracle's one-shot causal prefill (Sec. 4.2)."""
+    shape = _tiny_shape(dtype)
+    P, C = 256, 64
+    b_full = wl.Batch(prefill_slot=1, chunk_offset=0, chunk_len=P, decode_slots=np.zeros(0, np.int32),
+                      decode_ctx=np.zeros(0, np.int32))
+    inst = wl.make_instance(shape, b_full, max_seq_len=P, n_slots=2, seed=21)
+    ref = oracle.layer_forward(shape, inst.weights[0], inst.kv[0].copy(), oracle_batch(b_full), inst.x)
+    dm = DeviceModel(inst, max_tokens=C)
+    ys = []
+    for off in range(0, P, C):
+        b = wl.Batch(prefill_slot=1, chunk_offset=off, chunk_len=C, decode_slots=np.zeros(0, np.int32),
+                     decode_ctx=np.zeros(0, np.int32))
+        ys.append(from_dev(dm.layer(0, b, to_dev(inst.x[off:off + C], dtype))))
+    torch.cuda.synchronize()
+    err = rel_err(np.concatenate(ys), ref.y)
+    kv = from_dev(dm.kv_dev)[0, 1, :, :, :P]
+    kerr = rel_err(kv[0], ref.k_new.transpose(1, 0, 2))
+    verr = rel_err(kv[1], ref.v_new.transpose(1, 0, 2))
+    log(f"chunked prefill {dtype}: y {err:.3e} k {kerr:.3e} v {verr:.3e}")
+    assert max(err, kerr, verr) <= TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_model_step_consecutive_steps(dtype):
+    """Three consecutive decode-maximal steps through a 3-layer stack: chunks
+    at offsets 0, 64, 128 of a prompt, decodes advancing one position per
+    step, the KV grown in place by the library; compared with the oracle run
+    the same way on its own cache."""
+    shape = dataclasses.replace(_tiny_shape(dtype), n_layers=3)
+    L, Sx, n_slots = 3, 256, 6
+    b0 = wl.Batch(prefill_slot=2, chunk_offset=0, chunk_len=64, decode_slots=np.array([0, 4, 5, 1], np.int32),
+                  decode_ctx=np.array([10, 100, 0, 191], np.int32))
+    inst = wl.make_instance(shape, b0, max_seq_len=Sx, n_slots=n_slots, seed=31, n_layers=L)
+    dm = DeviceModel(inst)
+    okv = inst.kv.astype(np.float64)
+    rng = np.random.default_rng(5)
+    for step in range(3):
+        b = wl.Batch(prefill_slot=2, chunk_offset=64 * step, chunk_len=64, decode_slots=b0.decode_slots,
+                     decode_ctx=b0.decode_ctx + step)
+        xs = inst.x if step == 0 else (wl.round_to_bf16 if dtype == "bf16" else np.float32)(
+            rng.standard_normal(inst.x.shape).astype(np.float32))
+        xs = np.asarray(xs, np.float32)
+        before = bits_of(dm.kv_dev)
+        y = dm.step(b, to_dev(xs, dtype))
+        torch.cuda.synchronize()
+        outs = oracle.model_step(shape, inst.weights, okv, oracle_batch(b), xs)
+        after = bits_of(dm.kv_dev)
+        written = np.zeros(after.shape, bool)
+        for layer in range(L):
+            for s, p in zip(outs[layer].slots, outs[layer].positions):
+                written[layer, s, :, :, p, :] = True
+        assert np.array_equal(after[~written], before[~written]), "KV changed outside the new positions"
+        kvf = from_dev(dm.kv_dev)
+        err_kv = rel_err(kvf[written], okv[written])
+        err_y = rel_err(from_dev(y), outs[-1].y)
+        log(f"model_step {dtype} step {step}: y {err_y:.3e} kv {err_kv:.3e}")
+        assert err_y <= TOL[dtype] and err_kv <= TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_piggybacked_decode_equals_decode_alone(dtype):
+    """Sec. 4.3: a decode piggybacked on a chunk gives the same row as the same
+    decode run alone (both against the oracle and against each other)."""
+    shape = _tiny_shape(dtype)
+    b = wl.Batch(prefill_slot=0, chunk_offset=64, chunk_len=64, decode_slots=np.array([1, 2, 3], np.int32),
+                 decode_ctx=np.array([40, 200, 3], np.int32))
+    inst = wl.make_instance(shape, b, max_seq_len=256, n_slots=4, seed=41)
+    dm = DeviceModel(inst)
+    y_h = from_dev(dm.layer(0, b, to_dev(inst.x, dtype)))
+    for i in range(3):
+        dm.kv_dev.copy_(to_dev(inst.kv, dtype))
+        bi = wl.Batch(prefill_slot=-1, chunk_offset=0, chunk_len=0, decode_slots=b.decode_slots[i:i + 1],
+                      decode_ctx=b.decode_ctx[i:i + 1])
+        y_a = from_dev(dm.layer(0, bi, to_dev(inst.x[64 + i:65 + i], dtype)))
+        err = rel_err(y_h[64 + i:65 + i], y_a)
+        log(f"piggyback {dtype} decode {i}: {err:.3e}")
+        assert err <= TOL[dtype]
+
+
+# ============================================================================ paper-shaped workloads
+
+def test_layer_llama13b_workload():
+    run_and_check(wl.generate(wl.LLAMA13B_LAYER), "llama13b layer c256 b64")
+
+
+@pytest.mark.parametrize("chunk", [128, 256, 512])
+def test_layer_llama33b_workloads(chunk):
+    run_and_check(wl.generate(wl.llama33b_layer(chunk)), f"llama33b layer c{chunk} b32")
+
+
+def test_layer_gpt3_workload():
+    run_and_check(wl.generate(wl.GPT3_LAYER), "gpt3 layer c256 b27")
