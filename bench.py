@@ -71,6 +71,23 @@ def stage_work(shp, b, S_stats=None):
     return w
 
 
+def counter_traffic(stage: str, workload: str):
+    """HBM bytes per launch of a stage's kernel from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE record (profiles/traffic_<stage>_<workload>.json),
+    or None when there is no record or the kernel's source changed since."""
+    import hashlib
+    p = os.path.join(ROOT, "profiles", f"traffic_{stage}_{workload}.json")
+    if not os.path.exists(p):
+        return None
+    rec = json.load(open(p))
+    src = os.path.join(ROOT, rec["source"])
+    if not os.path.exists(src):
+        return None
+    if hashlib.sha256(open(src, "rb").read()).hexdigest()[:16] != rec["source_sha256_16"]:
+        return None
+    return round(rec["traffic_bytes"])
+
+
 BOUND = {"norm_1": "hbm", "preproj": "mfma", "rope_kv_append": "hbm", "chunk_attention": "mfma",
          "decode_attention": "hbm", "postproj": "mfma", "norm_2": "hbm", "ffn_ln1": "mfma", "ffn_ln2": "mfma"}
 
@@ -200,7 +217,7 @@ def main():
         roof = {"bound": "hbm", "achieved": dk["gbps"], "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                 "frac": dk["hbm_frac"]}
     roof["kernel"] = dom
-    roof["traffic"] = None
+    roof["traffic"] = counter_traffic(dom, w.name)
     lin = ["preproj", "postproj", "ffn_ln1", "ffn_ln2"]
     lin_ms = sum(kernels[k]["ms"] for k in lin if k in kernels)
     lin_flops = sum(work[k][0] for k in lin)
