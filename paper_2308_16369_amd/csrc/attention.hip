@@ -1,22 +1,23 @@
 // Attention of the hybrid batch, run separately for the prefill chunk and for
-// the decodes (Sec. 4.3).
+// the decodes (Sec. 4.3).  Both write per-split partial results
+// (max, sum, unnormalised o) that one combine pass merges per row.
 //
 // Chunked-prefill attention (bf16, MFMA): the chunk's queries at positions
 // off..off+C-1 attend to the prefill slot's keys 0..position (the earlier
-// chunks' cached keys plus, causally, the chunk's own; Sec. 4.2).  One block
-// = 64 queries of one head (4 waves x 16 rows); K and V tiles of 64 keys are
-// staged in LDS (V transposed so P*V reads 16 contiguous bytes per lane);
-// S = Q K^T and O += P V run on v_mfma_f32_16x16x32_bf16 with an fp32 online
-// softmax between them.
+// chunks' cached keys plus, causally, the chunk's own; Sec. 4.2).  Work item
+// = (64-query block, split of split_keys keys), one head per block of 4
+// waves x 16 query rows.  K and V tiles of 64 keys are staged in LDS (V
+// transposed so P*V reads 16 contiguous bytes per lane), the next tile is
+// prefetched into registers while the current one is used; S = Q K^T and
+// O += P V run on v_mfma_f32_16x16x32_bf16 with an fp32 online softmax.
 //
 // Row attention (decodes; in fp32 runs also the chunk rows): each row attends
-// to keys 0..pos of its slot.  Work item = (row, split of split_keys keys);
-// a block of 4 waves streams its split, each wave 64 keys per pass with
-// 16-byte loads (a key row spread over hd*size/16 lanes), partial dot
-// products reduce-scattered across those lanes so every lane ends up with one
-// key's score, wave-level online softmax, then P*V accumulated per lane.  The
-// block's four wave states are merged in LDS into one (max, sum, o) partial;
-// a combine pass merges the splits of each row.
+// to keys 0..pos of its slot.  Work item = (row, split of split_keys keys); a
+// block of 4 waves streams its split, each wave 64 keys per pass with 16-byte
+// loads (a key row spread over hd*size/16 lanes), partial dot products
+// reduce-scattered across those lanes so every lane ends up with one key's
+// score, wave-level online softmax, then P*V accumulated per lane.  The
+// block's four wave states are merged in LDS into one partial.
 #include "kernels.h"
 
 namespace sarathi {
@@ -27,23 +28,26 @@ constexpr float LOG2E = 1.4426950408889634f;
 template <int D>
 __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(PrefillArgs a, float scale_log2) {
   constexpr int KT = 64;                 // keys per tile
-  constexpr int DCH = D / 8;             // 16-byte chunks per K row
+  constexpr int DCH = D / 8;             // 16-byte chunks per K/V row
+  constexpr int LD = KT * DCH / 256;     // chunks of K (and of V) per thread per tile
   __shared__ uint4 ks_[KT * DCH];        // K tile [key][D], chunk ^ (key & 7)
   __shared__ uint4 vt_[D * (KT / 8)];    // V^T tile [d][KT keys], chunk ^ (d & 7)
   __shared__ uint4 ps_[4][16 * (KT / 8)];// per-wave P [16 rows][KT], chunk ^ (row & 7)
 
-  const int h = blockIdx.y;
-  const int q0 = blockIdx.x * 64;
+  const int item = blockIdx.x, h = blockIdx.y;
+  const int wv = a.work[item];
+  const int q0 = (wv >> 12) * 64, ksplit = wv & 4095;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const bf16* qkv = reinterpret_cast<const bf16*>(a.qkv);
   const bf16* cache = reinterpret_cast<const bf16*>(a.kv_layer);
   const bf16* kbase = cache + (size_t)a.slot * a.st.slot + (size_t)h * a.st.head;
   const bf16* vbase = kbase + a.st.kv;
 
-  // Keys this block needs: 0 .. off + min(q0 + 64, C) - 1.
-  const int q_end = min(q0 + 64, a.C);
-  const int n_keys = a.offset + q_end;
-  const int n_tiles = (n_keys + KT - 1) / KT;
+  // This item's keys: [kbeg, kend) within 0 .. off + min(q0 + 64, C) - 1.
+  const int n_keys = a.offset + min(q0 + 64, a.C);
+  const int kbeg = ksplit * a.split_keys;
+  const int kend = min(n_keys, kbeg + a.split_keys);
+  const int n_tiles = (kend - kbeg + KT - 1) / KT;
 
   // Q fragments (A operand): row = wave*16 + lane%16, d = ks*32 + 8*(lane/16).
   const int qrow = q0 + wave * 16 + (lane & 15);
@@ -66,25 +70,41 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(PrefillArgs a, f
 #pragma unroll
   for (int dt = 0; dt < D / 16; ++dt) o_acc[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  for (int kt = 0; kt < n_tiles; ++kt) {
-    const int k0 = kt * KT;
-    // ---- stage K (row-major) and V (transposed) tiles; keys past n_keys are zero.
-    for (int c = tid; c < KT * DCH; c += 256) {
-      const int key = c / DCH, ch = c % DCH;
-      const bool ok = k0 + key < n_keys;
-      const size_t off = (size_t)(k0 + key) * a.st.pos + ch * 8;
-      const uint4 kv4 = ok ? *reinterpret_cast<const uint4*>(kbase + off) : make_uint4(0, 0, 0, 0);
-      ks_[key * DCH + (ch ^ (key & 7))] = kv4;
-      const uint4 vv4 = ok ? *reinterpret_cast<const uint4*>(vbase + off) : make_uint4(0, 0, 0, 0);
-      const bf16* vv = reinterpret_cast<const bf16*>(&vv4);
-      bf16* vt = reinterpret_cast<bf16*>(vt_);
+  // Tile loads into registers; key addresses are clamped to the last key of
+  // the item (finite data; such keys are masked out of the softmax).
+  uint4 kreg[LD], vreg[LD];
+  auto gload = [&](int kt) {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int d = ch * 8 + j;
-        vt[(d * (KT / 8) + ((key >> 3) ^ (d & 7))) * 8 + (key & 7)] = vv[j];
+    for (int j = 0; j < LD; ++j) {
+      const int c = tid + 256 * j;
+      const int kp = min(kbeg + kt * KT + c / DCH, kend - 1);
+      const size_t off = (size_t)kp * a.st.pos + (c % DCH) * 8;
+      kreg[j] = *reinterpret_cast<const uint4*>(kbase + off);
+      vreg[j] = *reinterpret_cast<const uint4*>(vbase + off);
+    }
+  };
+  auto sstore = [&]() {
+    bf16* vt = reinterpret_cast<bf16*>(vt_);
+#pragma unroll
+    for (int j = 0; j < LD; ++j) {
+      const int c = tid + 256 * j;
+      const int key = c / DCH, ch = c % DCH;
+      ks_[key * DCH + (ch ^ (key & 7))] = kreg[j];
+      const bf16* vv = reinterpret_cast<const bf16*>(&vreg[j]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int d = ch * 8 + e;
+        vt[(d * (KT / 8) + ((key >> 3) ^ (d & 7))) * 8 + (key & 7)] = vv[e];
       }
     }
+  };
+
+  if (n_tiles > 0) gload(0);
+  for (int kt = 0; kt < n_tiles; ++kt) {
+    const int k0 = kbeg + kt * KT;
+    sstore();
     __syncthreads();
+    if (kt + 1 < n_tiles) gload(kt + 1);
 
     // ---- S = Q K^T for the wave's 16 rows x 64 keys.
     floatx4 s[KT / 16];
@@ -100,7 +120,7 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(PrefillArgs a, f
       }
     }
 
-    // ---- mask (key position <= query position), online softmax per row.
+    // ---- mask (key position <= query position, key in this item), online softmax.
     float p[KT / 16][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -108,7 +128,7 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(PrefillArgs a, f
 #pragma unroll
       for (int nt = 0; nt < KT / 16; ++nt) {
         const int kp = k0 + nt * 16 + (lane & 15);
-        const float v = (kp <= qpos[i] && kp < n_keys) ? s[nt][i] * scale_log2 : -INFINITY;
+        const float v = (kp <= qpos[i] && kp < kend) ? s[nt][i] * scale_log2 : -INFINITY;
         p[nt][i] = v;
         mx = fmaxf(mx, v);
       }
@@ -158,24 +178,26 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(PrefillArgs a, f
     __syncthreads();
   }
 
-  // ---- normalise and store rows < C.
-  bf16* out = reinterpret_cast<bf16*>(a.out);
+  // ---- partials of rows < C: [m, l, o[D]].
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int r = q0 + wave * 16 + 4 * (lane >> 4) + i;
-    if (r >= a.C) continue;
-    const float inv = 1.0f / l_run[i];
+    const int rb = wave * 16 + 4 * (lane >> 4) + i;
+    if (q0 + rb >= a.C) continue;
+    float* dst = a.part + ((size_t)(item * 64 + rb) * a.nh + h) * (D + 2);
+    if ((lane & 15) == 0) {
+      dst[0] = m_run[i];
+      dst[1] = l_run[i];
+    }
 #pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt)
-      out[(size_t)r * a.ld_out + h * D + dt * 16 + (lane & 15)] = f2bf(o_acc[dt][i] * inv);
+    for (int dt = 0; dt < D / 16; ++dt) dst[2 + dt * 16 + (lane & 15)] = o_acc[dt][i];
   }
 }
 
 hipError_t launch_attn_prefill(int dtype, const PrefillArgs& a, hipStream_t s) {
-  if (a.C <= 0) return hipSuccess;
+  if (a.C <= 0 || a.n_work <= 0) return hipSuccess;
   if (dtype != 1) return hipErrorInvalidValue;
   const float scale_log2 = LOG2E / sqrtf((float)a.hd);
-  dim3 grid((a.C + 63) / 64, a.nh);
+  dim3 grid(a.n_work, a.nh);
   if (a.hd == 128)
     hipLaunchKernelGGL(attn_prefill_bf16_kernel<128>, grid, dim3(256), 0, s, a, scale_log2);
   else
@@ -287,7 +309,7 @@ __global__ __launch_bounds__(256) void attn_rows_kernel(RowAttnArgs a, float sca
   __syncthreads();
   float M = fmaxf(fmaxf(red_m[0], red_m[1]), fmaxf(red_m[2], red_m[3]));
   const float Ms = (M == -INFINITY) ? 0.f : M;
-  float* dst = a.part + ((size_t)item * a.nh + h) * (D + 2);
+  float* dst = a.part + ((size_t)(a.part_base + item) * a.nh + h) * (D + 2);
   for (int d = tid; d < D; d += 256) {
     float acc = 0.f;
 #pragma unroll
@@ -303,44 +325,56 @@ __global__ __launch_bounds__(256) void attn_rows_kernel(RowAttnArgs a, float sca
   }
 }
 
-// Merge the splits of each row: O = sum_s o_s 2^(m_s - M) / sum_s l_s 2^(m_s - M).
 template <typename T, int D>
-__global__ __launch_bounds__(64) void attn_combine_kernel(RowAttnArgs a) {
+static hipError_t run_rows(const RowAttnArgs& a, hipStream_t s) {
+  const float scale_log2 = LOG2E / sqrtf((float)D);
+  hipLaunchKernelGGL((attn_rows_kernel<T, D>), dim3(a.n_work, a.nh), dim3(256), 0, s, a, scale_log2);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_rows(int dtype, const RowAttnArgs& a, hipStream_t s) {
+  if (a.n_work <= 0) return hipSuccess;
+  if (dtype == 0) return a.hd == 128 ? run_rows<float, 128>(a, s) : run_rows<float, 64>(a, s);
+  return a.hd == 128 ? run_rows<bf16, 128>(a, s) : run_rows<bf16, 64>(a, s);
+}
+
+// ============================================================================ combine
+// O = sum_s o_s 2^(m_s - M) / sum_s l_s 2^(m_s - M), M = max_s m_s.
+template <typename T, int D>
+__global__ __launch_bounds__(64) void attn_combine_kernel(CombineArgs a) {
   const int r = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
-  const int s0 = a.split0[r], s1 = a.split0[r + 1];
+  const int start = a.comb[3 * r], cnt = a.comb[3 * r + 1], stride = a.comb[3 * r + 2];
   float M = -INFINITY;
-  for (int s = s0; s < s1; ++s) M = fmaxf(M, a.part[((size_t)s * a.nh + h) * (D + 2)]);
+  for (int j = 0; j < cnt; ++j) M = fmaxf(M, a.part[((size_t)(start + j * stride) * a.nh + h) * (D + 2)]);
+  const float Ms = (M == -INFINITY) ? 0.f : M;
   float L = 0.f;
   float acc[D / 64];
 #pragma unroll
   for (int e = 0; e < D / 64; ++e) acc[e] = 0.f;
-  for (int s = s0; s < s1; ++s) {
-    const float* src = a.part + ((size_t)s * a.nh + h) * (D + 2);
-    const float w = exp2f(src[0] - M);
+  for (int j = 0; j < cnt; ++j) {
+    const float* src = a.part + ((size_t)(start + j * stride) * a.nh + h) * (D + 2);
+    const float w = exp2f(src[0] - Ms);
     L += src[1] * w;
 #pragma unroll
     for (int e = 0; e < D / 64; ++e) acc[e] += src[2 + lane + 64 * e] * w;
   }
   const float inv = 1.0f / L;
-  T* out = reinterpret_cast<T*>(a.out) + (size_t)(a.row_base + r) * a.ld_out + h * D;
+  T* out = reinterpret_cast<T*>(a.out) + (size_t)r * a.ld_out + h * D;
 #pragma unroll
   for (int e = 0; e < D / 64; ++e) out[lane + 64 * e] = from_f<T>(acc[e] * inv);
 }
 
-template <typename T, int D>
-static hipError_t run_rows(const RowAttnArgs& a, hipStream_t s) {
-  const float scale_log2 = LOG2E / sqrtf((float)D);
-  hipLaunchKernelGGL((attn_rows_kernel<T, D>), dim3(a.n_work, a.nh), dim3(256), 0, s, a, scale_log2);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attn_combine_kernel<T, D>), dim3(a.n_rows, a.nh), dim3(64), 0, s, a);
-  return hipGetLastError();
-}
-
-hipError_t launch_attn_rows(int dtype, const RowAttnArgs& a, hipStream_t s) {
+hipError_t launch_attn_combine(int dtype, const CombineArgs& a, hipStream_t s) {
   if (a.n_rows <= 0) return hipSuccess;
-  if (dtype == 0) return a.hd == 128 ? run_rows<float, 128>(a, s) : run_rows<float, 64>(a, s);
-  return a.hd == 128 ? run_rows<bf16, 128>(a, s) : run_rows<bf16, 64>(a, s);
+  dim3 grid(a.n_rows, a.nh);
+  if (dtype == 0) {
+    if (a.hd == 128) hipLaunchKernelGGL((attn_combine_kernel<float, 128>), grid, dim3(64), 0, s, a);
+    else hipLaunchKernelGGL((attn_combine_kernel<float, 64>), grid, dim3(64), 0, s, a);
+  } else {
+    if (a.hd == 128) hipLaunchKernelGGL((attn_combine_kernel<bf16, 128>), grid, dim3(64), 0, s, a);
+    else hipLaunchKernelGGL((attn_combine_kernel<bf16, 64>), grid, dim3(64), 0, s, a);
+  }
+  return hipGetLastError();
 }
 
 }  // namespace sarathi

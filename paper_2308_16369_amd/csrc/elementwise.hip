@@ -25,50 +25,88 @@ __device__ __forceinline__ float block_sum_256(float v, float* red) {
   return red[0] + red[1] + red[2] + red[3];
 }
 
-// One row per block.  RMS: x / sqrt(mean(x^2) + eps) * g.
+// One row per block, one read of the row: every thread keeps its 16-byte
+// chunks (at most NC of them) in registers across the reductions.
+// RMS: x / sqrt(mean(x^2) + eps) * g.
 // LayerNorm: (x - mean) / sqrt(mean((x - mean)^2) + eps) * g + b.
+template <typename T> struct Store16;
+template <> struct Store16<bf16> {
+  __device__ __forceinline__ static uint4 pack(const float* f) {
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f2bf(f[2 * i]) | ((uint32_t)f2bf(f[2 * i + 1]) << 16);
+    return make_uint4(w[0], w[1], w[2], w[3]);
+  }
+};
+template <> struct Store16<float> {
+  __device__ __forceinline__ static uint4 pack(const float* f) {
+    return make_uint4(__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]), __float_as_uint(f[3]));
+  }
+};
+
+constexpr int NORM_NC = 12;   // units per thread
+
+// A unit is CE = max(16 bytes of input, 16 bytes of output) elements, so
+// loads and stores are whole 16-byte vectors; H up to NORM_NC * 256 * CE.
 template <typename Tin, typename Tout, bool LAYER>
 __global__ __launch_bounds__(256) void norm_kernel(const Tin* __restrict__ in, const Tout* __restrict__ g,
                                                    const Tout* __restrict__ b, Tout* __restrict__ out,
                                                    float* __restrict__ copy_f32, int H, float eps) {
   __shared__ float red[4];
+  constexpr int EI = Vec16<Tin>::N, EO = Vec16<Tout>::N;
+  constexpr int CE = EI > EO ? EI : EO;
   const size_t row = blockIdx.x;
   const Tin* x = in + row * (size_t)H;
-  constexpr int E = Vec16<Tin>::N;
-  const int nchunk = H / E;
-  float mean = 0.f;
-  if (LAYER) {
-    float s = 0.f;
-    for (int c = threadIdx.x; c < nchunk; c += 256) {
-      float f[E];
-      Vec16<Tin>::unpack(reinterpret_cast<const uint4*>(x)[c], f);
+  const int nunit = H / CE;
+  float v[NORM_NC][CE];
+  float s = 0.f;
 #pragma unroll
-      for (int e = 0; e < E; ++e) s += f[e];
+  for (int j = 0; j < NORM_NC; ++j) {
+    const int u = threadIdx.x + 256 * j;
+    if (u < nunit) {
+#pragma unroll
+      for (int o = 0; o < CE; o += EI) Vec16<Tin>::unpack(*reinterpret_cast<const uint4*>(x + u * CE + o), &v[j][o]);
+#pragma unroll
+      for (int e = 0; e < CE; ++e) s += v[j][e];
+    } else {
+#pragma unroll
+      for (int e = 0; e < CE; ++e) v[j][e] = 0.f;
     }
-    mean = block_sum_256(s, red) / (float)H;
   }
+  float mean = 0.f;
+  if (LAYER) mean = block_sum_256(s, red) / (float)H;
   float ss = 0.f;
-  for (int c = threadIdx.x; c < nchunk; c += 256) {
-    float f[E];
-    Vec16<Tin>::unpack(reinterpret_cast<const uint4*>(x)[c], f);
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const float d = f[e] - mean;
-      ss += d * d;
+  for (int j = 0; j < NORM_NC; ++j) {
+    if (threadIdx.x + 256 * j < nunit) {
+#pragma unroll
+      for (int e = 0; e < CE; ++e) {
+        const float d = v[j][e] - mean;
+        ss += d * d;
+      }
     }
   }
   const float r = 1.0f / sqrtf(block_sum_256(ss, red) / (float)H + eps);
   Tout* y = out + row * (size_t)H;
-  for (int c = threadIdx.x; c < nchunk; c += 256) {
-    float f[E];
-    Vec16<Tin>::unpack(reinterpret_cast<const uint4*>(x)[c], f);
+  float* cp = copy_f32 ? copy_f32 + row * (size_t)H : nullptr;
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const int i = c * E + e;
-      float v = (f[e] - mean) * r * to_f<Tout>(g[i]);
-      if (LAYER) v += to_f<Tout>(b[i]);
-      y[i] = from_f<Tout>(v);
-      if (copy_f32) copy_f32[row * (size_t)H + i] = f[e];
+  for (int j = 0; j < NORM_NC; ++j) {
+    const int u = threadIdx.x + 256 * j;
+    if (u >= nunit) continue;
+    const int i0 = u * CE;
+#pragma unroll
+    for (int o = 0; o < CE; o += EO) {
+      float gv[EO], bv[EO], f[EO];
+      Vec16<Tout>::unpack(*reinterpret_cast<const uint4*>(g + i0 + o), gv);
+      if (LAYER) Vec16<Tout>::unpack(*reinterpret_cast<const uint4*>(b + i0 + o), bv);
+#pragma unroll
+      for (int e = 0; e < EO; ++e) f[e] = (v[j][o + e] - mean) * r * gv[e] + (LAYER ? bv[e] : 0.f);
+      *reinterpret_cast<uint4*>(y + i0 + o) = Store16<Tout>::pack(f);
+    }
+    if (cp) {
+#pragma unroll
+      for (int o = 0; o < CE; o += 4)
+        *reinterpret_cast<float4*>(cp + i0 + o) = make_float4(v[j][o], v[j][o + 1], v[j][o + 2], v[j][o + 3]);
     }
   }
 }
@@ -117,10 +155,12 @@ __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a, int heads_
   float q0 = to_f<T>(q[i]), q1 = to_f<T>(q[i + half]);
   float k0 = to_f<T>(k[i]), k1 = to_f<T>(k[i + half]);
   if (a.rope) {
-    const double theta = pow((double)a.base, -2.0 * (double)i / (double)a.hd);
-    double sd, cd;
-    sincos((double)pos * theta, &sd, &cd);
-    const float c = (float)cd, sn = (float)sd;
+    // angle pos * base^(-2i/hd), reduced to [-pi, pi] in fp64, sin/cos in fp32
+    const double theta = exp2(-2.0 * (double)i / (double)a.hd * log2((double)a.base));
+    const double ang = (double)pos * theta;
+    const double red = ang - 6.283185307179586 * rint(ang * 0.15915494309189535);
+    float sn, c;
+    __sincosf((float)red, &sn, &c);
     const float nq0 = q0 * c - q1 * sn, nq1 = q0 * sn + q1 * c;
     const float nk0 = k0 * c - k1 * sn, nk1 = k0 * sn + k1 * c;
     q0 = nq0; q1 = nq1; k0 = nk0; k1 = nk1;

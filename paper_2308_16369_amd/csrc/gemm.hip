@@ -46,13 +46,27 @@ __device__ __forceinline__ void epi_store(const GemmP& p, int r, int c, float v)
 }
 
 // ============================================================================ bf16 MFMA
-template <int BM, int BN, int EPI>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmP p) {
+// Block tile BM x BN (W rows) x 64, WGM x WGN waves, PD register stages of
+// prefetch.  Loads are unconditional (addresses clamped into the operands) so
+// the compiler can keep PD tiles in flight with partial vmcnt waits; rows and
+// k-chunks outside the operands are zeroed when the registers are written to
+// LDS.  The k-loop runs whole groups of U tiles (tiles past the end are zero
+// and add nothing), keeping every register-stage index static.
+__device__ __forceinline__ uint4 mask4(const uint4& v, bool ok) {
+  return make_uint4(ok ? v.x : 0u, ok ? v.y : 0u, ok ? v.z : 0u, ok ? v.w : 0u);
+}
+
+template <int BM, int BN, int WGM, int WGN, int PD, int EPI>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_kernel(GemmP p) {
+  constexpr int NT = 64 * WGM * WGN;
   constexpr int BK = 64;
-  constexpr int WTM = BM / 2, WTN = BN / 2;
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;
   constexpr int FM = WTM / 16, FN = WTN / 16;
-  constexpr int AL = BM / 32, BL = BN / 32;
-  static_assert(BM % 32 == 0 && BN % 64 == 0, "tile");
+  constexpr int RPL = NT / 8;                  // rows covered by one 16-byte load per thread
+  constexpr int AL = BM / RPL, BL = BN / RPL;
+  constexpr int U = (PD % 2 == 0) ? PD : 2 * PD;
+  static_assert(BM % RPL == 0 && BN % RPL == 0, "load split");
+  static_assert(WTM % 16 == 0 && WTN % 16 == 0 && (EPI != EPI_SWIGLU || FN % 2 == 0), "wave tile");
   extern __shared__ uint4 lds[];   // [2][(BM + BN) * 8] 16-byte chunks
 
   // XCD-aware order: block b runs on XCD b % 8.  Consecutive tiles (the
@@ -67,7 +81,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmP p) {
   const int tile_n = rest / p.n_split;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WGN, wn = wave % WGN;
   const int m0 = tile_m * BM;
   const int n0_out = tile_n * (EPI == EPI_SWIGLU ? BN / 2 : BN);
   const int kbeg = split * p.k_split;
@@ -82,17 +96,18 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmP p) {
   bool a_ok[AL];
 #pragma unroll
   for (int i = 0; i < AL; ++i) {
-    const int r = m0 + lr + 32 * i;
+    const int r = m0 + lr + RPL * i;
     a_ok[i] = r < p.M;
-    a_src[i] = A + (size_t)(a_ok[i] ? r : 0) * p.K + kbeg + lc * 8;
+    a_src[i] = A + (size_t)(a_ok[i] ? r : 0) * p.K;
   }
   const bf16* b_src[BL];
   bool b_ok[BL];
 #pragma unroll
   for (int i = 0; i < BL; ++i) {
-    const int nl = lr + 32 * i;
+    const int nl = lr + RPL * i;
     int wrow;
     if (EPI == EPI_SWIGLU) {
+      // each wave's WTN columns: first half gate rows, second half up rows
       const int q = nl / WTN, w = nl % WTN, half = WTN / 2;
       const int j = n0_out + q * half + (w % half);
       b_ok[i] = j < p.N;
@@ -101,30 +116,30 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmP p) {
       wrow = n0_out + nl;
       b_ok[i] = wrow < p.N;
     }
-    b_src[i] = W + (size_t)(b_ok[i] ? wrow : 0) * p.K + kbeg + lc * 8;
+    b_src[i] = W + (size_t)(b_ok[i] ? wrow : 0) * p.K;
   }
 
-  uint4 ra[AL], rb[BL];
-  auto gload = [&](int kt) {
+  uint4 R[PD][AL + BL];
+  auto gload = [&](uint4* r, int kt) {
+    const int kc = min(kt, nk - 1);
+    const int kk = min(kbeg + kc * BK + lc * 8, p.K - 8);
+#pragma unroll
+    for (int i = 0; i < AL; ++i) r[i] = *reinterpret_cast<const uint4*>(a_src[i] + kk);
+#pragma unroll
+    for (int i = 0; i < BL; ++i) r[AL + i] = *reinterpret_cast<const uint4*>(b_src[i] + kk);
+  };
+  auto sstore = [&](int buf, const uint4* r, int kt) {
+    uint4* s = lds + buf * (BM + BN) * 8;
     const bool kok = kbeg + kt * BK + lc * 8 < kend;
 #pragma unroll
-    for (int i = 0; i < AL; ++i)
-      ra[i] = (a_ok[i] && kok) ? *reinterpret_cast<const uint4*>(a_src[i] + kt * BK) : make_uint4(0, 0, 0, 0);
-#pragma unroll
-    for (int i = 0; i < BL; ++i)
-      rb[i] = (b_ok[i] && kok) ? *reinterpret_cast<const uint4*>(b_src[i] + kt * BK) : make_uint4(0, 0, 0, 0);
-  };
-  auto sstore = [&](int buf) {
-    uint4* s = lds + buf * (BM + BN) * 8;
-#pragma unroll
     for (int i = 0; i < AL; ++i) {
-      const int r = lr + 32 * i;
-      s[r * 8 + (lc ^ (r & 7))] = ra[i];
+      const int row = lr + RPL * i;
+      s[row * 8 + (lc ^ (row & 7))] = mask4(r[i], a_ok[i] && kok);
     }
 #pragma unroll
     for (int i = 0; i < BL; ++i) {
-      const int r = BM + lr + 32 * i;
-      s[r * 8 + (lc ^ (r & 7))] = rb[i];
+      const int row = BM + lr + RPL * i;
+      s[row * 8 + (lc ^ (row & 7))] = mask4(r[AL + i], b_ok[i] && kok);
     }
   };
 
@@ -134,15 +149,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmP p) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  if (nk > 0) {
-    gload(0);
-    sstore(0);
-  }
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) gload(kt + 1);
-    const uint4* s = lds + cur * (BM + BN) * 8;
+  auto compute = [&](int buf) {
+    const uint4* s = lds + buf * (BM + BN) * 8;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       const int ch = ks * 4 + (lane >> 4);
@@ -163,8 +171,24 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmP p) {
         for (int fn = 0; fn < FN; ++fn)
           acc[fm][fn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[fm], bfr[fn], acc[fm][fn], 0, 0, 0);
     }
-    if (kt + 1 < nk) sstore(cur ^ 1);
+  };
+
+  if (nk > 0) {
+#pragma unroll
+    for (int st = 0; st < PD; ++st) gload(R[st], st);
+    sstore(0, R[0], 0);
+    gload(R[0], PD);
     __syncthreads();
+    for (int kb = 0; kb < nk; kb += U) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int kt = kb + u;
+        compute(u & 1);
+        sstore((u + 1) & 1, R[(u + 1) % PD], kt + 1);
+        gload(R[(u + 1) % PD], kt + 1 + PD);
+        __syncthreads();
+      }
+    }
   }
 
   // Epilogue.  acc[fm][fn][i] = C[row 4*(lane/16)+i][col lane%16] of the 16x16 tile.
@@ -266,30 +290,34 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmP p) {
 }
 
 // ============================================================================ launch
-template <int BM, int BN, int EPI>
+// Tile configurations of the bf16 kernel (BM x BN W rows, waves, prefetch stages).
+enum TileCfg { CFG_160x128 = 0, CFG_320x128 = 1, CFG_64x128 = 2, CFG_96x128 = 3 };
+
+template <int BM, int BN, int WGM, int WGN, int PD, int EPI>
 static hipError_t run_bf16(GemmP p, hipStream_t s) {
   const size_t lds_bytes = 2 * (BM + BN) * 8 * sizeof(uint4);
-  static bool attr_set = false;   // per process; the attribute is per function
+  static bool attr_set = false;   // the attribute is per kernel function
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)gemm_bf16_kernel<BM, BN, EPI>,
+    hipError_t e = hipFuncSetAttribute((const void*)gemm_bf16_kernel<BM, BN, WGM, WGN, PD, EPI>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
   const int grid = (p.n_tiles + 7) / 8 * 8;
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, EPI>), dim3(grid), dim3(256), lds_bytes, s, p);
+  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WGM, WGN, PD, EPI>), dim3(grid), dim3(64 * WGM * WGN), lds_bytes,
+                     s, p);
   return hipGetLastError();
 }
 
-template <int BM>
+template <int BM, int BN, int WGM, int WGN, int PD>
 static hipError_t run_bf16_epi(int epi, const GemmP& p, hipStream_t s) {
   switch (epi) {
-    case EPI_STORE: return run_bf16<BM, 128, EPI_STORE>(p, s);
-    case EPI_GELU: return run_bf16<BM, 128, EPI_GELU>(p, s);
-    case EPI_SWIGLU: return run_bf16<BM, 128, EPI_SWIGLU>(p, s);
-    case EPI_RESID_TO_F32: return run_bf16<BM, 128, EPI_RESID_TO_F32>(p, s);
-    case EPI_RESIDF32_TO_ACT: return run_bf16<BM, 128, EPI_RESIDF32_TO_ACT>(p, s);
-    default: return run_bf16<BM, 128, EPI_ATOMIC>(p, s);
+    case EPI_STORE: return run_bf16<BM, BN, WGM, WGN, PD, EPI_STORE>(p, s);
+    case EPI_GELU: return run_bf16<BM, BN, WGM, WGN, PD, EPI_GELU>(p, s);
+    case EPI_SWIGLU: return run_bf16<BM, BN, WGM, WGN, PD, EPI_SWIGLU>(p, s);
+    case EPI_RESID_TO_F32: return run_bf16<BM, BN, WGM, WGN, PD, EPI_RESID_TO_F32>(p, s);
+    case EPI_RESIDF32_TO_ACT: return run_bf16<BM, BN, WGM, WGN, PD, EPI_RESIDF32_TO_ACT>(p, s);
+    default: return run_bf16<BM, BN, WGM, WGN, PD, EPI_ATOMIC>(p, s);
   }
 }
 
@@ -301,16 +329,29 @@ static hipError_t run_f32(const GemmP& p, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Block rows for the bf16 kernel: the candidate that pads M least, larger on ties.
-static int pick_bm(int M) {
-  if (M <= 64) return 64;
-  const int cands[3] = {160, 128, 96};
-  int best = 160, best_pad = 1 << 30;
-  for (int c : cands) {
-    const int pad = (M + c - 1) / c * c;
-    if (pad < best_pad) { best_pad = pad; best = c; }
+static int cfg_bm(int cfg) {
+  switch (cfg) {
+    case CFG_320x128: return 320;
+    case CFG_64x128: return 64;
+    case CFG_96x128: return 96;
+    default: return 160;
   }
-  return best;
+}
+
+// Tile choice for the skinny matmuls of the hybrid batch (M = C + B rows).
+// Many W panels (>= 180 tiles of 128 rows) and M in (160, 320]: one block
+// covers all rows (W read once per block, 8 waves).  A middle count: 160-row
+// blocks.  Few panels (postproj / ffn_ln2 at N = hidden): 64-row blocks,
+// split-K below.  Small M: the block height that pads M least.
+static int pick_cfg(int M, int n_panels) {
+  if (M <= 64) return CFG_64x128;
+  if (M <= 96) return CFG_96x128;
+  if (n_panels >= 180 && M > 160 && M <= 320) return CFG_320x128;
+  if (n_panels >= 100) {
+    const int pad160 = (M + 159) / 160 * 160, pad96 = (M + 95) / 96 * 96;
+    return pad96 < pad160 ? CFG_96x128 : CFG_160x128;
+  }
+  return CFG_64x128;
 }
 
 hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s) {
@@ -330,9 +371,13 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s) {
     }
   }
 
-  const int BM = pick_bm(a.M), BN = 128;
+  constexpr int BN = 128;
+  const int out_per_tile = (a.kind == LIN_SWIGLU) ? BN / 2 : BN;
+  const int n_panels = (a.N + out_per_tile - 1) / out_per_tile;
+  const int cfg = pick_cfg(a.M, n_panels);
+  const int BM = cfg_bm(cfg);
   p.tiles_m = (a.M + BM - 1) / BM;
-  p.tiles_n = (a.kind == LIN_SWIGLU) ? (a.N + BN / 2 - 1) / (BN / 2) : (a.N + BN - 1) / BN;
+  p.tiles_n = n_panels;
   int epi;
   switch (a.kind) {
     case LIN_PLAIN: epi = EPI_STORE; break;
@@ -344,24 +389,23 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s) {
   // Split-K for the residual ops when the tile grid leaves CUs idle: fp32
   // partials are added atomically into an accumulator that starts out holding
   // the residual (LIN_RESID: the fp32 output itself; LIN_RESID_F32IN: a.acc,
-  // cast to the output afterwards).
+  // cast to the output afterwards).  Each split covers whole groups of two
+  // 64-wide k-tiles.
   const int tiles = p.tiles_m * p.tiles_n;
   const bool resid_kind = a.kind == LIN_RESID || a.kind == LIN_RESID_F32IN;
   const bool can_split = resid_kind && a.allow_split && (a.kind == LIN_RESID || a.acc != nullptr);
-  if (can_split && tiles < 160) {
-    int ns = (240 + tiles - 1) / tiles;
-    const int max_ns = a.K / 256 > 0 ? a.K / 256 : 1;
-    if (ns > max_ns) ns = max_ns;
+  if (can_split && tiles < 256) {
+    const int kgroups = (a.K + 127) / 128;
+    int ns = (400 + tiles - 1) / tiles;
+    if (ns > kgroups / 2) ns = kgroups / 2;
     if (ns > 1) {
-      const int kt = (a.K + 63) / 64;
-      const int kt_per = (kt + ns - 1) / ns;
-      p.k_split = kt_per * 64;
-      p.n_split = (kt + kt_per - 1) / kt_per;
+      const int g_per = (kgroups + ns - 1) / ns;
+      p.k_split = g_per * 128;
+      p.n_split = (a.K + p.k_split - 1) / p.k_split;
       epi = EPI_ATOMIC;
       float* accbuf = (a.kind == LIN_RESID) ? reinterpret_cast<float*>(a.out) : a.acc;
       if (!a.acc_ready) {
-        hipError_t e = launch_to_f32(a.kind == LIN_RESID ? dtype : 0, a.resid, accbuf,
-                                     (size_t)a.M * a.N, s);
+        hipError_t e = launch_to_f32(a.kind == LIN_RESID ? dtype : 0, a.resid, accbuf, (size_t)a.M * a.N, s);
         if (e != hipSuccess) return e;
       }
       p.out = accbuf;
@@ -369,11 +413,11 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s) {
   }
   p.n_tiles = p.tiles_m * p.tiles_n * p.n_split;
   hipError_t e;
-  switch (BM) {
-    case 64: e = run_bf16_epi<64>(epi, p, s); break;
-    case 96: e = run_bf16_epi<96>(epi, p, s); break;
-    case 128: e = run_bf16_epi<128>(epi, p, s); break;
-    default: e = run_bf16_epi<160>(epi, p, s); break;
+  switch (cfg) {
+    case CFG_320x128: e = run_bf16_epi<320, 128, 4, 2, 2>(epi, p, s); break;
+    case CFG_64x128: e = run_bf16_epi<64, 128, 2, 2, 2>(epi, p, s); break;
+    case CFG_96x128: e = run_bf16_epi<96, 128, 2, 2, 2>(epi, p, s); break;
+    default: e = run_bf16_epi<160, 128, 2, 2, 2>(epi, p, s); break;
   }
   if (e != hipSuccess) return e;
   if (epi == EPI_ATOMIC && a.kind == LIN_RESID_F32IN)

@@ -53,19 +53,23 @@ struct LinearArgs {
 hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s);
 
 // ---- attention
+// Partial results (one per row x head x key split): [m, l, o[hd]] in fp32,
+// m the running max of the log2-scaled scores, l the sum of 2^(s - m),
+// o the unnormalised weighted sum of values.
 struct PrefillArgs {
   const void* qkv;      // chunk rows 0..C-1, q columns rotated
   int ld_qkv;
   const void* kv_layer;
   KVStrides st;
   int slot, offset, C, nh, hd;
-  void* out;            // [T, nh*hd], chunk rows 0..C-1
-  int ld_out;
+  const int* work;      // [n_work] (q_block << 12) | key_split
+  int n_work, split_keys;
+  float* part;          // item i, row j of its q-block -> partial index i * 64 + j
 };
 hipError_t launch_attn_prefill(int dtype, const PrefillArgs& a, hipStream_t s);
 
-// Row attention: each row r in [row_base, T) attends to keys 0..row_pos[r]
-// of slot row_slot[r], split into work items of split_keys keys.
+// Row attention: each row r in [row_base, row_base + n_rows) attends to keys
+// 0..row_pos[r] of slot row_slot[r], split into work items of split_keys keys.
 struct RowAttnArgs {
   const void* qkv;
   int ld_qkv;
@@ -73,14 +77,22 @@ struct RowAttnArgs {
   KVStrides st;
   const int* row_slot;
   const int* row_pos;
-  const int* split0;    // [n_rows + 1] first work item of each row
   const int* work;      // [n_work] (row_rel << 12) | split
-  int row_base, n_rows, n_work, split_keys, nh, hd;
-  float* part;          // [n_work, nh, hd + 2]
-  void* out;
-  int ld_out;
+  int row_base, n_work, split_keys, nh, hd;
+  float* part;          // work item w -> partial index part_base + w
+  int part_base;
 };
 hipError_t launch_attn_rows(int dtype, const RowAttnArgs& a, hipStream_t s);
+
+// Combine: row r's partials are comb[3r] + j * comb[3r + 2] for j < comb[3r + 1].
+struct CombineArgs {
+  const float* part;
+  const int* comb;
+  int n_rows, nh, hd;
+  void* out;            // [n_rows, nh * hd]
+  int ld_out;
+};
+hipError_t launch_attn_combine(int dtype, const CombineArgs& a, hipStream_t s);
 
 // fp32 accumulator -> dtype
 hipError_t launch_cast_out(int dtype, const float* acc, void* out, size_t n, hipStream_t s);

@@ -46,7 +46,9 @@ int hip_fail(hipError_t e, const char* what) {
   return fail(SARATHI_EHIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-constexpr int SPLIT_KEYS = 256;   // keys per row-attention work item
+constexpr int SPLIT_KEYS = 256;   // keys per decode-attention work item
+constexpr int PRE_SPLIT = 256;    // keys per chunk-attention work item
+constexpr int QBLOCK = 64;        // chunk rows per chunk-attention work item
 
 size_t esize(const sarathi_model_cfg* c) { return c->dtype == SARATHI_BF16 ? 2 : 4; }
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -60,6 +62,9 @@ int check_cfg(const sarathi_model_cfg* c) {
     return fail(SARATHI_EUNSUPPORTED, "head_dim %d not supported (64 or 128)", c->head_dim);
   if (c->hidden <= 0 || c->hidden % 8) return fail(SARATHI_EUNSUPPORTED, "hidden %d must be a positive multiple of 8", c->hidden);
   if (c->ffn <= 0 || c->ffn % 8) return fail(SARATHI_EUNSUPPORTED, "ffn %d must be a positive multiple of 8", c->ffn);
+  // the norm kernels keep a row in registers: 12 x 256 x 8 (bf16) or x 4 (fp32) elements
+  const int max_hidden = c->dtype == SARATHI_BF16 ? 24576 : 12288;
+  if (c->hidden > max_hidden) return fail(SARATHI_EUNSUPPORTED, "hidden %d > %d", c->hidden, max_hidden);
   if (c->n_heads <= 0 || c->n_heads > 65535) return fail(SARATHI_EUNSUPPORTED, "n_heads %d out of range", c->n_heads);
   if (c->n_layers <= 0) return fail(SARATHI_EINVAL, "n_layers %d must be positive", c->n_layers);
   if (c->norm != SARATHI_NORM_RMS && c->norm != SARATHI_NORM_LAYER) return fail(SARATHI_EUNSUPPORTED, "norm %d", c->norm);
@@ -78,7 +83,6 @@ bool same_cfg(const sarathi_model_cfg* a, const sarathi_model_cfg* b) {
 
 struct Layout {
   size_t a, qkv, o, hres, m, yacc, part, meta, ping0, ping1, total;
-  int max_work;
 };
 
 Layout make_layout(const sarathi_model_cfg* c, int T, int S) {
@@ -93,9 +97,10 @@ Layout make_layout(const sarathi_model_cfg* c, int T, int S) {
   L.hres = take(T * H * 4);
   L.m = take(T * F * es);
   L.yacc = take(T * H * 4);
-  L.max_work = T * ((S + SPLIT_KEYS - 1) / SPLIT_KEYS);
-  L.part = take((size_t)L.max_work * c->n_heads * (c->head_dim + 2) * 4);
-  L.meta = take(((size_t)T * 3 + 1 + L.max_work) * 4);
+  const size_t max_pre = (size_t)((T + QBLOCK - 1) / QBLOCK) * ((S + PRE_SPLIT - 1) / PRE_SPLIT);
+  const size_t max_dec = (size_t)T * ((S + SPLIT_KEYS - 1) / SPLIT_KEYS);
+  L.part = take((max_pre * QBLOCK + max_dec) * c->n_heads * (c->head_dim + 2) * 4);
+  L.meta = take(((size_t)T * 5 + max_pre + max_dec) * 4);
   L.ping0 = take(T * H * es);
   L.ping1 = take(T * H * es);
   L.total = off;
@@ -104,9 +109,9 @@ Layout make_layout(const sarathi_model_cfg* c, int T, int S) {
 
 // Host-side description of the batch and its device metadata.
 struct Plan {
-  int C, B, T, row_base, n_rows, n_work;
-  std::vector<int> meta;          // row_slot[T] row_pos[T] split0[n_rows+1] work[n_work]
-  size_t o_slot, o_pos, o_split0, o_work;   // int offsets into meta
+  int C, B, T, row_base, n_pre, n_dec;
+  std::vector<int> meta;   // row_slot[T] row_pos[T] comb[3T] pre_work[n_pre] dec_work[n_dec]
+  size_t o_slot, o_pos, o_comb, o_pre, o_dec;   // int offsets into meta
 };
 
 int check_batch(const sarathi_model_cfg* cfg, const sarathi_kv* kv, const sarathi_hybrid_batch* b) {
@@ -145,28 +150,43 @@ Plan make_plan(const sarathi_model_cfg* cfg, const sarathi_hybrid_batch* b) {
   p.C = b->chunk_len;
   p.B = b->n_decodes;
   p.T = p.C + p.B;
-  // bf16: the chunk goes to the MFMA prefill kernel, the decodes to row
-  // attention.  fp32: every row goes to row attention (a chunk row at
-  // position p is attention over keys 0..p, like a decode with ctx = p).
+  // bf16: the chunk goes to the MFMA chunk-attention kernel (work item =
+  // 64-row query block x key split), the decodes to row attention (work item
+  // = row x key split).  fp32: every row goes to row attention (a chunk row
+  // at position p is attention over keys 0..p, like a decode with ctx = p).
   p.row_base = (cfg->dtype == SARATHI_BF16) ? p.C : 0;
-  p.n_rows = p.T - p.row_base;
-  std::vector<int> slot(p.T), pos(p.T);
+  std::vector<int> slot(p.T), pos(p.T), comb(3 * p.T), pre, dec;
   for (int r = 0; r < p.C; ++r) { slot[r] = b->prefill_slot; pos[r] = b->chunk_offset + r; }
   for (int i = 0; i < p.B; ++i) { slot[p.C + i] = b->decode_slots[i]; pos[p.C + i] = b->decode_ctx_lens[i]; }
-  std::vector<int> split0(p.n_rows + 1), work;
-  for (int r = 0; r < p.n_rows; ++r) {
-    split0[r] = (int)work.size();
-    const int nk = pos[p.row_base + r] + 1;
-    const int ns = (nk + SPLIT_KEYS - 1) / SPLIT_KEYS;
-    for (int s = 0; s < ns; ++s) work.push_back((r << 12) | s);
+  if (p.row_base > 0) {
+    for (int qb = 0; qb * QBLOCK < p.C; ++qb) {
+      const int n_keys = b->chunk_offset + std::min((qb + 1) * QBLOCK, p.C);
+      const int ns = (n_keys + PRE_SPLIT - 1) / PRE_SPLIT;
+      const int first = (int)pre.size();
+      for (int s = 0; s < ns; ++s) pre.push_back((qb << 12) | s);
+      for (int r = qb * QBLOCK; r < std::min((qb + 1) * QBLOCK, p.C); ++r) {
+        comb[3 * r] = first * QBLOCK + (r - qb * QBLOCK);
+        comb[3 * r + 1] = ns;
+        comb[3 * r + 2] = QBLOCK;
+      }
+    }
   }
-  split0[p.n_rows] = (int)work.size();
-  p.n_work = (int)work.size();
-  p.meta.reserve(3 * p.T + 1 + work.size());
+  const int pre_rows = (int)pre.size() * QBLOCK;
+  for (int r = p.row_base; r < p.T; ++r) {
+    const int ns = (pos[r] + 1 + SPLIT_KEYS - 1) / SPLIT_KEYS;
+    comb[3 * r] = pre_rows + (int)dec.size();
+    comb[3 * r + 1] = ns;
+    comb[3 * r + 2] = 1;
+    for (int s = 0; s < ns; ++s) dec.push_back(((r - p.row_base) << 12) | s);
+  }
+  p.n_pre = (int)pre.size();
+  p.n_dec = (int)dec.size();
+  p.meta.reserve(5 * p.T + pre.size() + dec.size());
   p.o_slot = 0; p.meta.insert(p.meta.end(), slot.begin(), slot.end());
   p.o_pos = p.meta.size(); p.meta.insert(p.meta.end(), pos.begin(), pos.end());
-  p.o_split0 = p.meta.size(); p.meta.insert(p.meta.end(), split0.begin(), split0.end());
-  p.o_work = p.meta.size(); p.meta.insert(p.meta.end(), work.begin(), work.end());
+  p.o_comb = p.meta.size(); p.meta.insert(p.meta.end(), comb.begin(), comb.end());
+  p.o_pre = p.meta.size(); p.meta.insert(p.meta.end(), pre.begin(), pre.end());
+  p.o_dec = p.meta.size(); p.meta.insert(p.meta.end(), dec.begin(), dec.end());
   return p;
 }
 
@@ -175,10 +195,13 @@ int check_weights(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, 
   const void* need[] = {w->norm1_g, w->w_qkv, w->w_o, w->norm2_g, w->w_up, w->w_down};
   for (const void* p : need)
     if (!p) return fail(SARATHI_EINVAL, "layer %d: a weight pointer is NULL", layer);
-  if (cfg->norm == SARATHI_NORM_LAYER && (!w->norm1_b || !w->norm2_b))
-    return fail(SARATHI_EINVAL, "layer %d: LayerNorm biases are NULL", layer);
-  for (const void* p : {w->w_qkv, w->w_o, w->w_up, w->w_down})
-    if (!aligned16(p)) return fail(SARATHI_EINVAL, "layer %d: weight matrices must be 16-byte aligned", layer);
+  for (const void* p : need)
+    if (!aligned16(p)) return fail(SARATHI_EINVAL, "layer %d: weights must be 16-byte aligned", layer);
+  if (cfg->norm == SARATHI_NORM_LAYER) {
+    if (!w->norm1_b || !w->norm2_b) return fail(SARATHI_EINVAL, "layer %d: LayerNorm biases are NULL", layer);
+    if (!aligned16(w->norm1_b) || !aligned16(w->norm2_b))
+      return fail(SARATHI_EINVAL, "layer %d: weights must be 16-byte aligned", layer);
+  }
   return SARATHI_OK;
 }
 
@@ -265,27 +288,32 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
   e = launch_rope_append(dt, ra, c.s);
   if (e != hipSuccess) return hip_fail(e, "rope/kv append");
 
-  // attention: the chunk and the decodes separately
+  // attention: the chunk and the decodes separately, then one combine pass
   SARATHI_MARK();
-  if (dt == SARATHI_BF16 && P.C > 0) {
+  float* part = reinterpret_cast<float*>(ws + c.L.part);
+  if (P.n_pre > 0) {
     PrefillArgs pa{};
     pa.qkv = ws + c.L.qkv; pa.ld_qkv = 3 * QD; pa.kv_layer = kv_layer; pa.st = c.kv->st;
     pa.slot = c.plan->meta[P.o_slot]; pa.offset = c.plan->meta[P.o_pos]; pa.C = P.C; pa.nh = nh; pa.hd = hd;
-    pa.out = ws + c.L.o; pa.ld_out = QD;
+    pa.work = meta + P.o_pre; pa.n_work = P.n_pre; pa.split_keys = PRE_SPLIT; pa.part = part;
     e = launch_attn_prefill(dt, pa, c.s);
-    if (e != hipSuccess) return hip_fail(e, "prefill attention");
+    if (e != hipSuccess) return hip_fail(e, "chunk attention");
   }
   SARATHI_MARK();
-  if (P.n_rows > 0) {
+  if (P.n_dec > 0) {
     RowAttnArgs da{};
     da.qkv = ws + c.L.qkv; da.ld_qkv = 3 * QD; da.kv_layer = kv_layer; da.st = c.kv->st;
-    da.row_slot = meta + P.o_slot; da.row_pos = meta + P.o_pos; da.split0 = meta + P.o_split0;
-    da.work = meta + P.o_work; da.row_base = P.row_base; da.n_rows = P.n_rows; da.n_work = P.n_work;
-    da.split_keys = SPLIT_KEYS; da.nh = nh; da.hd = hd;
-    da.part = reinterpret_cast<float*>(ws + c.L.part); da.out = ws + c.L.o; da.ld_out = QD;
+    da.row_slot = meta + P.o_slot; da.row_pos = meta + P.o_pos; da.work = meta + P.o_dec;
+    da.row_base = P.row_base; da.n_work = P.n_dec; da.split_keys = SPLIT_KEYS; da.nh = nh; da.hd = hd;
+    da.part = part; da.part_base = P.n_pre * QBLOCK;
     e = launch_attn_rows(dt, da, c.s);
     if (e != hipSuccess) return hip_fail(e, "decode attention");
   }
+  CombineArgs ca{};
+  ca.part = part; ca.comb = meta + P.o_comb; ca.n_rows = T; ca.nh = nh; ca.hd = hd; ca.out = ws + c.L.o;
+  ca.ld_out = QD;
+  e = launch_attn_combine(dt, ca, c.s);
+  if (e != hipSuccess) return hip_fail(e, "attention combine");
 
   // postproj + residual -> hres (fp32)
   SARATHI_MARK();
