@@ -13,10 +13,10 @@
 //
 // Row attention (decodes; in fp32 runs also the chunk rows): each row attends
 // to keys 0..pos of its slot.  Work item = (row, split of split_keys keys); a
-// block of 4 waves streams its split, each wave 64 keys per pass with 16-byte
+// block of 4 waves streams its split, each wave 32 keys per pass with 16-byte
 // loads (a key row spread over hd*size/16 lanes), partial dot products
-// reduce-scattered across those lanes so every lane ends up with one key's
-// score, wave-level online softmax, then P*V accumulated per lane.  The
+// reduce-scattered across those lanes so each key's score ends up in two
+// lanes, wave-level online softmax, then P*V accumulated per lane.  The
 // block's four wave states are merged in LDS into one partial.
 #include "kernels.h"
 
@@ -25,19 +25,44 @@ namespace sarathi {
 constexpr float LOG2E = 1.4426950408889634f;
 
 // ============================================================================ prefill (bf16, MFMA)
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+
+// LDS transpose read (gfx950): within each group of 16 lanes, output lane j
+// element e is element (j % 4) of the 8 bytes addressed by lane 4e + j / 4.
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+__device__ __forceinline__ uint2 lds_read_tr16(const void* p) {
+  const v4i16 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p));
+  return __builtin_bit_cast(uint2, v);
+}
+
+// One block = one head x (64 queries of the chunk, one split of keys); wave w
+// owns queries w*16..w*16+15.  Per 64-key tile:
+//   S^T = K Q^T  (MFMA: A = K rows from LDS, B = the wave's Q fragments), so
+//     each lane holds 16 scores of ONE query (lane % 16) for keys
+//     nt*16 + 4*(lane/16) + i;
+//   the online softmax runs on that query's own registers (+2 lane shuffles);
+//   O^T += V^T P^T (MFMA: B = the lane's probabilities packed as bf16x8
+//     straight from registers; A = V^T fragments read from the row-major V
+//     tile with LDS transpose reads).  The k order of this product is a
+//     permutation of the 32 keys of a block: lane group g holds keys
+//     4g..4g+3 and 16+4g..16+4g+3, which is what two transpose reads of rows
+//     4g..4g+3 and 16+4g..16+4g+3 deliver.
+// K and V tiles are stored row-major (16-byte chunks XOR-swizzled by row),
+// double-buffered in LDS; the next tile is prefetched into registers while the
+// current one is used; one barrier per tile.
 template <int D>
 __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(PrefillArgs a, float scale_log2) {
   constexpr int KT = 64;                 // keys per tile
   constexpr int DCH = D / 8;             // 16-byte chunks per K/V row
   constexpr int LD = KT * DCH / 256;     // chunks of K (and of V) per thread per tile
-  __shared__ uint4 ks_[KT * DCH];        // K tile [key][D], chunk ^ (key & 7)
-  __shared__ uint4 vt_[D * (KT / 8)];    // V^T tile [d][KT keys], chunk ^ (d & 7)
-  __shared__ uint4 ps_[4][16 * (KT / 8)];// per-wave P [16 rows][KT], chunk ^ (row & 7)
+  __shared__ u32x4 ks_[2][KT * DCH];     // K tile [key][D], chunk ^ (key & 7)
+  __shared__ u32x4 vs_[2][KT * DCH];     // V tile [key][D], chunk ^ (key & 7)
 
   const int item = blockIdx.x, h = blockIdx.y;
   const int wv = a.work[item];
   const int q0 = (wv >> 12) * 64, ksplit = wv & 4095;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int grp = lane >> 4, ql = lane & 15;
   const bf16* qkv = reinterpret_cast<const bf16*>(a.qkv);
   const bf16* cache = reinterpret_cast<const bf16*>(a.kv_layer);
   const bf16* kbase = cache + (size_t)a.slot * a.st.slot + (size_t)h * a.st.head;
@@ -49,147 +74,146 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(PrefillArgs a, f
   const int kend = min(n_keys, kbeg + a.split_keys);
   const int n_tiles = (kend - kbeg + KT - 1) / KT;
 
-  // Q fragments (A operand): row = wave*16 + lane%16, d = ks*32 + 8*(lane/16).
-  const int qrow = q0 + wave * 16 + (lane & 15);
-  uint4 qf[D / 32];
+  // The lane's query (B operand of S^T): q = ql, d = ks*32 + 8*grp.
+  const int myq = q0 + wave * 16 + ql;
+  const int qpos = a.offset + myq;
+  u32x4 qf[D / 32];
 #pragma unroll
-  for (int ks = 0; ks < D / 32; ++ks)
-    qf[ks] = (qrow < a.C) ? *reinterpret_cast<const uint4*>(qkv + (size_t)qrow * a.ld_qkv + h * D + ks * 32 + 8 * (lane >> 4))
-                          : make_uint4(0, 0, 0, 0);
-
-  // Rows held by this lane in the C layout: 4*(lane/16) + i of the wave's 16.
-  float m_run[4], l_run[4];
-  int qpos[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    m_run[i] = -INFINITY;
-    l_run[i] = 0.f;
-    qpos[i] = a.offset + q0 + wave * 16 + 4 * (lane >> 4) + i;
+  for (int ks = 0; ks < D / 32; ++ks) {
+    const u32x4 v = *reinterpret_cast<const u32x4*>(qkv + (size_t)min(myq, a.C - 1) * a.ld_qkv + h * D + ks * 32 + 8 * grp);
+    qf[ks] = (myq < a.C) ? v : u32x4{0u, 0u, 0u, 0u};
   }
-  floatx4 o_acc[D / 16];
+
+  float m_run = -INFINITY, l_run = 0.f;
+  floatx4 o_acc[D / 16];                 // O^T[d = dt*16 + 4*grp + i][q = ql]
 #pragma unroll
   for (int dt = 0; dt < D / 16; ++dt) o_acc[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  // Tile loads into registers; key addresses are clamped to the last key of
-  // the item (finite data; such keys are masked out of the softmax).
-  uint4 kreg[LD], vreg[LD];
+  // Tile loads into registers; key addresses are clamped to the item's last
+  // key (finite data; such keys are masked out of the softmax).
+  u32x4 kreg[LD], vreg[LD];
   auto gload = [&](int kt) {
+    const int k0 = kbeg + kt * KT;
 #pragma unroll
     for (int j = 0; j < LD; ++j) {
       const int c = tid + 256 * j;
-      const int kp = min(kbeg + kt * KT + c / DCH, kend - 1);
-      const size_t off = (size_t)kp * a.st.pos + (c % DCH) * 8;
-      kreg[j] = *reinterpret_cast<const uint4*>(kbase + off);
-      vreg[j] = *reinterpret_cast<const uint4*>(vbase + off);
+      const size_t off = (size_t)min(k0 + c / DCH, kend - 1) * a.st.pos + (c % DCH) * 8;
+      kreg[j] = *reinterpret_cast<const u32x4*>(kbase + off);
+      vreg[j] = *reinterpret_cast<const u32x4*>(vbase + off);
     }
   };
-  auto sstore = [&]() {
-    bf16* vt = reinterpret_cast<bf16*>(vt_);
+  auto sstore = [&](int buf) {
 #pragma unroll
     for (int j = 0; j < LD; ++j) {
       const int c = tid + 256 * j;
       const int key = c / DCH, ch = c % DCH;
-      ks_[key * DCH + (ch ^ (key & 7))] = kreg[j];
-      const bf16* vv = reinterpret_cast<const bf16*>(&vreg[j]);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int d = ch * 8 + e;
-        vt[(d * (KT / 8) + ((key >> 3) ^ (d & 7))) * 8 + (key & 7)] = vv[e];
-      }
+      ks_[buf][key * DCH + (ch ^ (key & 7))] = kreg[j];
+      vs_[buf][key * DCH + (ch ^ (key & 7))] = vreg[j];
     }
   };
 
-  if (n_tiles > 0) gload(0);
-  for (int kt = 0; kt < n_tiles; ++kt) {
-    const int k0 = kbeg + kt * KT;
-    sstore();
-    __syncthreads();
-    if (kt + 1 < n_tiles) gload(kt + 1);
+  // Transpose-read addressing of V^T fragments: lane i of group grp reads 8
+  // bytes of row 4*grp + i/4 (+16 for the second half) at columns
+  // dt*16 + 4*(i%4) .. +3.
+  const int tr_row = 4 * grp + (ql >> 2);
+  const int tr_c16 = (ql & 3) >> 1;      // 16-byte chunk within the 16 columns of dt
+  const int tr_half = (ql & 1) * 8;      // byte offset inside the chunk
 
-    // ---- S = Q K^T for the wave's 16 rows x 64 keys.
+  if (n_tiles > 0) {
+    gload(0);
+    sstore(0);
+  }
+  __syncthreads();
+  for (int kt = 0; kt < n_tiles; ++kt) {
+    const int buf = kt & 1;
+    const int k0 = kbeg + kt * KT;
+    if (kt + 1 < n_tiles) gload(kt + 1);
+    // keep the next tile's loads in flight across this tile's work: the
+    // scheduler would otherwise hoist the LDS stores (and their waits) up here
+    __builtin_amdgcn_sched_barrier(0);
+
+    // ---- S^T = K Q^T: s[nt][i] = score of key k0 + nt*16 + 4*grp + i for query ql.
     floatx4 s[KT / 16];
 #pragma unroll
     for (int nt = 0; nt < KT / 16; ++nt) {
       s[nt] = floatx4{0.f, 0.f, 0.f, 0.f};
-      const int key = nt * 16 + (lane & 15);
+      const int key = nt * 16 + ql;
 #pragma unroll
       for (int ks = 0; ks < D / 32; ++ks) {
-        const int ch = ks * 4 + (lane >> 4);
-        const bf16x8_t kf = __builtin_bit_cast(bf16x8_t, ks_[key * DCH + (ch ^ (key & 7))]);
-        s[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, qf[ks]), kf, s[nt], 0, 0, 0);
+        const int ch = ks * 4 + grp;
+        const bf16x8_t kf = __builtin_bit_cast(bf16x8_t, ks_[buf][key * DCH + (ch ^ (key & 7))]);
+        s[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, __builtin_bit_cast(bf16x8_t, qf[ks]), s[nt], 0, 0, 0);
       }
     }
 
-    // ---- mask (key position <= query position, key in this item), online softmax.
-    float p[KT / 16][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float mx = -INFINITY;
-#pragma unroll
-      for (int nt = 0; nt < KT / 16; ++nt) {
-        const int kp = k0 + nt * 16 + (lane & 15);
-        const float v = (kp <= qpos[i] && kp < kend) ? s[nt][i] * scale_log2 : -INFINITY;
-        p[nt][i] = v;
-        mx = fmaxf(mx, v);
-      }
-#pragma unroll
-      for (int m = 8; m >= 1; m >>= 1) mx = fmaxf(mx, __shfl_xor(mx, m, 64));
-      const float m_new = fmaxf(m_run[i], mx);
-      const float m_safe = (m_new == -INFINITY) ? 0.f : m_new;
-      const float corr = exp2f(m_run[i] - m_safe);
-      float sum = 0.f;
-#pragma unroll
-      for (int nt = 0; nt < KT / 16; ++nt) {
-        const float e = exp2f(p[nt][i] - m_safe);
-        p[nt][i] = e;
-        sum += e;
-      }
-#pragma unroll
-      for (int m = 8; m >= 1; m >>= 1) sum += __shfl_xor(sum, m, 64);
-      l_run[i] = l_run[i] * corr + sum;
-      m_run[i] = m_new;
-#pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) o_acc[dt][i] *= corr;
-    }
-
-    // ---- P (bf16) to the wave's LDS slab, row-major [16][KT].
-    bf16* pw = reinterpret_cast<bf16*>(ps_[wave]);
+    // ---- mask (key position <= query position, key inside the item), online softmax.
+    float mx = -INFINITY;
 #pragma unroll
     for (int nt = 0; nt < KT / 16; ++nt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int r = 4 * (lane >> 4) + i, key = nt * 16 + (lane & 15);
-        pw[(r * (KT / 8) + ((key >> 3) ^ (r & 7))) * 8 + (key & 7)] = f2bf(p[nt][i]);
+        const int kp = k0 + nt * 16 + 4 * grp + i;
+        const float v = (kp <= qpos && kp < kend) ? s[nt][i] * scale_log2 : -INFINITY;
+        s[nt][i] = v;
+        mx = fmaxf(mx, v);
       }
-    __syncthreads();
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float m_new = fmaxf(m_run, mx);
+    const float m_safe = (m_new == -INFINITY) ? 0.f : m_new;
+    const float corr = exp2f(m_run - m_safe);
+    float sum = 0.f;
+#pragma unroll
+    for (int nt = 0; nt < KT / 16; ++nt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        s[nt][i] = exp2f(s[nt][i] - m_safe);
+        sum += s[nt][i];
+      }
+    sum += __shfl_xor(sum, 16, 64);
+    sum += __shfl_xor(sum, 32, 64);
+    l_run = l_run * corr + sum;
+    m_run = m_new;
+#pragma unroll
+    for (int dt = 0; dt < D / 16; ++dt) o_acc[dt] *= corr;
 
-    // ---- O += P V.
+    // ---- O^T += V^T P^T over two 32-key blocks.
+    const char* vb = reinterpret_cast<const char*>(vs_[buf]);
 #pragma unroll
     for (int kk = 0; kk < KT / 32; ++kk) {
-      const int r = lane & 15, ch = kk * 4 + (lane >> 4);
-      const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, ps_[wave][r * (KT / 8) + (ch ^ (r & 7))]);
+      u32x4 pw;
+      pw.x = (uint32_t)f2bf(s[2 * kk][0]) | ((uint32_t)f2bf(s[2 * kk][1]) << 16);
+      pw.y = (uint32_t)f2bf(s[2 * kk][2]) | ((uint32_t)f2bf(s[2 * kk][3]) << 16);
+      pw.z = (uint32_t)f2bf(s[2 * kk + 1][0]) | ((uint32_t)f2bf(s[2 * kk + 1][1]) << 16);
+      pw.w = (uint32_t)f2bf(s[2 * kk + 1][2]) | ((uint32_t)f2bf(s[2 * kk + 1][3]) << 16);
+      const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, pw);
+      const int r0 = kk * 32 + tr_row, r1 = r0 + 16;
 #pragma unroll
       for (int dt = 0; dt < D / 16; ++dt) {
-        const int d = dt * 16 + (lane & 15);
-        const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, vt_[d * (KT / 8) + (ch ^ (d & 7))]);
-        o_acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pf, vf, o_acc[dt], 0, 0, 0);
+        const int c16 = 2 * dt + tr_c16;
+        const uint2 lo = lds_read_tr16(vb + (r0 * DCH + (c16 ^ (r0 & 7))) * 16 + tr_half);
+        const uint2 hi = lds_read_tr16(vb + (r1 * DCH + (c16 ^ (r1 & 7))) * 16 + tr_half);
+        const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, u32x4{lo.x, lo.y, hi.x, hi.y});
+        o_acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o_acc[dt], 0, 0, 0);
       }
     }
+    __builtin_amdgcn_sched_barrier(0);
+    if (kt + 1 < n_tiles) sstore(buf ^ 1);
     __syncthreads();
   }
 
-  // ---- partials of rows < C: [m, l, o[D]].
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int rb = wave * 16 + 4 * (lane >> 4) + i;
-    if (q0 + rb >= a.C) continue;
+  // ---- partial of the lane's query (rows < C): [m, l, o[D]].
+  const int rb = wave * 16 + ql;
+  if (q0 + rb < a.C) {
     float* dst = a.part + ((size_t)(item * 64 + rb) * a.nh + h) * (D + 2);
-    if ((lane & 15) == 0) {
-      dst[0] = m_run[i];
-      dst[1] = l_run[i];
+    if (grp == 0) {
+      dst[0] = m_run;
+      dst[1] = l_run;
     }
 #pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt) dst[2 + dt * 16 + (lane & 15)] = o_acc[dt][i];
+    for (int dt = 0; dt < D / 16; ++dt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) dst[2 + dt * 16 + 4 * grp + i] = o_acc[dt][i];
   }
 }
 
@@ -206,13 +230,14 @@ hipError_t launch_attn_prefill(int dtype, const PrefillArgs& a, hipStream_t s) {
 }
 
 // ============================================================================ row attention
-template <typename T, int D>
+template <typename T, int D, int DUP>
 __global__ __launch_bounds__(256) void attn_rows_kernel(RowAttnArgs a, float scale_log2) {
   constexpr int EPL = Vec16<T>::N;           // elements per lane per key (16 bytes)
   constexpr int LPK = D / EPL;               // lanes per key row
   constexpr int KPI = 64 / LPK;              // keys per wave load instruction
-  constexpr int NI = LPK;                    // load instructions per pass (64 keys)
-  static_assert(LPK * KPI == 64 && NI * KPI == 64, "pass");
+  constexpr int NI = LPK / DUP;              // load instructions per pass
+  constexpr int KP = NI * KPI;               // keys per pass per wave (64 / DUP)
+  static_assert(LPK * KPI == 64 && NI * DUP == LPK, "pass");
   __shared__ float red_m[4], red_l[4];
   __shared__ float red_o[4][D];
 
@@ -242,15 +267,21 @@ __global__ __launch_bounds__(256) void attn_rows_kernel(RowAttnArgs a, float sca
 #pragma unroll
   for (int e = 0; e < EPL; ++e) o[e] = 0.f;
 
-  for (int pb = kb + wave * 64; pb < ke; pb += 256) {
+  // Each wave takes passes of KP keys (pb, pb + 4*KP, ...).  All K loads are
+  // issued first, then all V loads: the scores wait only for K (loads
+  // complete in order) while V is still in flight.  Key addresses past the
+  // split are clamped to its last key (finite data, masked below).
+  for (int pb = kb + wave * KP; pb < ke; pb += 4 * KP) {
     uint4 kr[NI], vr[NI];
 #pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const int key = pb + i * KPI + g;
-      const bool ok = key < ke;
-      kr[i] = ok ? *reinterpret_cast<const uint4*>(kbase + (size_t)key * a.st.pos) : make_uint4(0, 0, 0, 0);
-      vr[i] = ok ? *reinterpret_cast<const uint4*>(vbase + (size_t)key * a.st.pos) : make_uint4(0, 0, 0, 0);
-    }
+    for (int i = 0; i < NI; ++i)
+      kr[i] = *reinterpret_cast<const uint4*>(kbase + (size_t)min(pb + i * KPI + g, ke - 1) * a.st.pos);
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+      vr[i] = *reinterpret_cast<const uint4*>(vbase + (size_t)min(pb + i * KPI + g, ke - 1) * a.st.pos);
+    // Keep all 2*NI loads in flight before any use (the scheduler would
+    // otherwise sink each load next to its first use and serialise them).
+    __builtin_amdgcn_sched_barrier(0);
     float part[NI];
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
@@ -261,10 +292,11 @@ __global__ __launch_bounds__(256) void attn_rows_kernel(RowAttnArgs a, float sca
       for (int e = 0; e < EPL; ++e) acc = fmaf(q[e], kf[e], acc);
       part[i] = acc;
     }
-    // Reduce-scatter across the LPK lanes of a key group: after it, lane j
-    // holds the full score of the key loaded by instruction j.
+    // Reduce-scatter across the LPK lanes of a key group: afterwards the
+    // DUP lanes j with j / DUP == i hold the full score of the key loaded
+    // by instruction i.
 #pragma unroll
-    for (int n = NI, msk = LPK / 2; msk >= 1; n >>= 1, msk >>= 1) {
+    for (int n = NI, msk = LPK / 2; n > 1; n >>= 1, msk >>= 1) {
 #pragma unroll
       for (int idx = 0; idx < n / 2; ++idx) {
         const bool upper = (j & msk) != 0;
@@ -273,19 +305,22 @@ __global__ __launch_bounds__(256) void attn_rows_kernel(RowAttnArgs a, float sca
         part[idx] = keep + __shfl_xor(send, msk, 64);
       }
     }
-    const int mykey = pb + j * KPI + g;
+#pragma unroll
+    for (int msk = DUP / 2; msk >= 1; msk >>= 1) part[0] += __shfl_xor(part[0], msk, 64);
+    const int mykey = pb + (j / DUP) * KPI + g;
+    const bool own = (j % DUP) == 0;            // one lane per key counts in the sum
     const float sc = (mykey < ke) ? part[0] : -INFINITY;
     const float m_new = fmaxf(m_run, wave_max(sc));
     const float m_safe = (m_new == -INFINITY) ? 0.f : m_new;
     const float corr = exp2f(m_run - m_safe);
     const float pk = (mykey < ke) ? exp2f(sc - m_safe) : 0.f;
-    l_run = l_run * corr + wave_sum(pk);
+    l_run = l_run * corr + wave_sum(own ? pk : 0.f);
     m_run = m_new;
 #pragma unroll
     for (int e = 0; e < EPL; ++e) o[e] *= corr;
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
-      const float w = __shfl(pk, g * LPK + i, 64);
+      const float w = __shfl(pk, g * LPK + i * DUP, 64);
       float vf[EPL];
       Vec16<T>::unpack(vr[i], vf);
 #pragma unroll
@@ -328,7 +363,7 @@ __global__ __launch_bounds__(256) void attn_rows_kernel(RowAttnArgs a, float sca
 template <typename T, int D>
 static hipError_t run_rows(const RowAttnArgs& a, hipStream_t s) {
   const float scale_log2 = LOG2E / sqrtf((float)D);
-  hipLaunchKernelGGL((attn_rows_kernel<T, D>), dim3(a.n_work, a.nh), dim3(256), 0, s, a, scale_log2);
+  hipLaunchKernelGGL((attn_rows_kernel<T, D, 2>), dim3(a.n_work, a.nh), dim3(256), 0, s, a, scale_log2);
   return hipGetLastError();
 }
 
