@@ -40,7 +40,72 @@ def parse():
     ap.add_argument("--no-compare", action="store_true", help="skip the prefill-only / decode-only runs")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB elementwise copy kernel (for HBM counter scaling)")
+    ap.add_argument("--no-stack", action="store_true",
+                    help="skip the 40-layer model-step measurement (the 'stack' object)")
+    ap.add_argument("--stack-steps", type=int, default=5)
     return ap.parse_args()
+
+
+def bench_stack(steps: int, warmup: int):
+    """Model step of the 40-layer LLaMA-13B-shaped stack (chunk 256 + 48
+    decodes of context U[512, 2048], KV for 49 slots x 2112 positions):
+    time per step, per layer, and the decode accounting of Sec. 5.1.1 against
+    prefill-only and decode-only steps of the same rows."""
+    import numpy as np
+    import torch
+
+    import workloads as wl
+    from workloads.stack import generate_stack_on_device
+    from paper_2308_16369_amd import sarathi as S
+    from paper_2308_16369_amd import accounting
+
+    w = wl.LLAMA13B_STACK
+    shp = w.shape
+    st = generate_stack_on_device(w)
+    L = shp.n_layers
+    cfg = S.make_cfg(hidden=shp.hidden, n_heads=shp.n_heads, head_dim=shp.head_dim, ffn=shp.ffn, n_layers=L,
+                     rope_base=shp.rope_base, eps=shp.eps, dtype=S.BF16)
+    kv = S.sarathi_kv_alloc(cfg, st.kv.shape[1], st.kv.shape[4], st.kv.data_ptr(), st.kv.numel() * 2)
+    wabi = [S.make_weights({k: t.data_ptr() for k, t in lw.items()}) for lw in st.weights]
+    b = st.batch
+    T, C, B = b.n_tokens, b.chunk_len, b.n_decodes
+    ws_bytes = S.sarathi_workspace_bytes(cfg, T, B, st.kv.shape[4])
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def run(batch, x, steps_, warmup_):
+        bb, keep = S.make_batch(batch.prefill_slot, batch.chunk_offset, batch.chunk_len, list(batch.decode_slots),
+                                list(batch.decode_ctx))
+        y = torch.empty_like(x)
+        call = lambda: S.sarathi_model_step(cfg, wabi, kv, bb, x.data_ptr(), y.data_ptr(), ws.data_ptr(), ws_bytes,
+                                            stream.cuda_stream)
+        for _ in range(warmup_):
+            call()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps_):
+            call()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps_
+
+    ms = run(b, st.x, steps, warmup)
+    bp = wl.Batch(b.prefill_slot, b.chunk_offset, C, np.zeros(0, np.int32), np.zeros(0, np.int32))
+    bd = wl.Batch(-1, 0, 0, b.decode_slots, b.decode_ctx)
+    ms_p = run(bp, st.x[:C].clone(), steps, 1)
+    ms_d = run(bd, st.x[C:].clone(), steps, 1)
+    t_h = accounting.decode_time_per_token_hybrid(ms, ms_p, B)
+    t_b = accounting.decode_time_per_token_baseline(ms_d, B)
+    out = {"workload": w.name, "layers": L, "rows": T, "ms_per_step": round(ms, 4),
+           "tokens_per_s": round(T / (ms * 1e-3), 1), "ms_per_layer": round(ms / L, 5),
+           "prefill_only_ms_per_step": round(ms_p, 4), "decode_only_ms_per_step": round(ms_d, 4),
+           "decode_tokens_per_s_hybrid": round(1e3 / t_h, 1) if t_h > 0 else None,
+           "decode_tokens_per_s_decode_only": round(1e3 / t_b, 1),
+           "decode_speedup": round(t_b / t_h, 3) if t_h > 0 else None}
+    del st, ws
+    torch.cuda.empty_cache()
+    return out
 
 
 def stage_work(shp, b, S_stats=None):
@@ -243,6 +308,15 @@ def main():
                "sample": f"one full layer call of the same workload ({T} rows), float64 NumPy, median of "
                          f"{len(times)} runs of {t_cpu:.2f}s; host affinity {len(os.sched_getaffinity(0))} cpus"}
 
+    stack = None
+    if not args.no_stack:
+        del kv_t, wdev, ws
+        torch.cuda.empty_cache()
+        t_s = time.time()
+        stack = bench_stack(args.stack_steps, 2)
+        print(f"# stack measured in {time.time() - t_s:.1f}s: {stack['ms_per_step']} ms per step",
+              file=sys.stderr, flush=True)
+
     value = T / (ms_plain * 1e-3)
     line = {
         "metric": "hybrid-batch tokens/s per layer (C+B rows per layer forward)",
@@ -268,6 +342,7 @@ def main():
                        "weight_stream_hbm_frac": round(lin_bytes / (lin_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)},
         "kernels": kernels,
         **extra,
+        "stack": stack,
     }
     print(json.dumps(line), flush=True)
 

@@ -161,10 +161,14 @@ int sarathi_kv_get_strides(const sarathi_kv* kv, sarathi_kv_strides* out);
  *   o    [T, nh*hd]             dtype   attention output
  *   hres [T, hidden]            fp32    x + postproj(o)
  *   m    [T, ffn]               dtype   ffn_ln1 activation output
- * For sarathi_model_step they hold the last layer's values.
+ *   ping[2] [T, hidden]         dtype   sarathi_model_step hands layer l's
+ *                                       output to layer l+1 in ping[(l+1) % 2]
+ * For sarathi_model_step they hold the last layer's values (so ping[(L-1) % 2]
+ * holds the last layer's input when L > 1).
  */
 typedef struct {
   size_t a, qkv, o, hres, m;
+  size_t ping[2];
   size_t total;      /* bytes needed */
 } sarathi_ws_layout;
 
@@ -222,8 +226,11 @@ int sarathi_model_step(const sarathi_model_cfg* cfg, const sarathi_layer_weights
  *   SARATHI_LINEAR_SWIGLU  out[M,N] (dtype) = silu(x Wg^T) * (x Wu^T), W = [Wg; Wu] [2N, K]
  *   SARATHI_LINEAR_GELU    out[M,N] (dtype) = gelu(x W^T)
  * x [M,K] dtype row-major, W [N or 2N, K] dtype; K multiple of 8.
- * `scratch`/`scratch_bytes`: device memory for split-K accumulation; bytes
- * needed = sarathi_linear_scratch_bytes(M, N) (may be 0 for NULL).
+ * `scratch`/`scratch_bytes`: device memory (16-byte aligned) for split-K
+ * partials of the two residual kinds; with NULL or too small a buffer the op
+ * runs without split-K (same result up to fp32 summation order, lower
+ * occupancy at small M).  sarathi_linear_scratch_bytes(M, N) is the most it
+ * can use (4 splits of M x N fp32).  Results are deterministic either way.
  */
 #define SARATHI_LINEAR_PLAIN        0
 #define SARATHI_LINEAR_RESID        1

@@ -50,8 +50,8 @@ constexpr int NORM_NC = 12;   // units per thread
 // loads and stores are whole 16-byte vectors; H up to NORM_NC * 256 * CE.
 template <typename Tin, typename Tout, bool LAYER>
 __global__ __launch_bounds__(256) void norm_kernel(const Tin* __restrict__ in, const Tout* __restrict__ g,
-                                                   const Tout* __restrict__ b, Tout* __restrict__ out,
-                                                   float* __restrict__ copy_f32, int H, float eps) {
+                                                   const Tout* __restrict__ b, Tout* __restrict__ out, int H,
+                                                   float eps) {
   __shared__ float red[4];
   constexpr int EI = Vec16<Tin>::N, EO = Vec16<Tout>::N;
   constexpr int CE = EI > EO ? EI : EO;
@@ -88,7 +88,6 @@ __global__ __launch_bounds__(256) void norm_kernel(const Tin* __restrict__ in, c
   }
   const float r = 1.0f / sqrtf(block_sum_256(ss, red) / (float)H + eps);
   Tout* y = out + row * (size_t)H;
-  float* cp = copy_f32 ? copy_f32 + row * (size_t)H : nullptr;
 #pragma unroll
   for (int j = 0; j < NORM_NC; ++j) {
     const int u = threadIdx.x + 256 * j;
@@ -103,35 +102,29 @@ __global__ __launch_bounds__(256) void norm_kernel(const Tin* __restrict__ in, c
       for (int e = 0; e < EO; ++e) f[e] = (v[j][o + e] - mean) * r * gv[e] + (LAYER ? bv[e] : 0.f);
       *reinterpret_cast<uint4*>(y + i0 + o) = Store16<Tout>::pack(f);
     }
-    if (cp) {
-#pragma unroll
-      for (int o = 0; o < CE; o += 4)
-        *reinterpret_cast<float4*>(cp + i0 + o) = make_float4(v[j][o], v[j][o + 1], v[j][o + 2], v[j][o + 3]);
-    }
   }
 }
 
 template <typename Tin, typename Tout>
-static void norm_dispatch(bool layer, const void* in, const void* g, const void* b, void* out,
-                          float* copy_f32, int rows, int H, float eps, hipStream_t s) {
+static void norm_dispatch(bool layer, const void* in, const void* g, const void* b, void* out, int rows, int H,
+                          float eps, hipStream_t s) {
   if (layer)
     hipLaunchKernelGGL((norm_kernel<Tin, Tout, true>), dim3(rows), dim3(256), 0, s, (const Tin*)in,
-                       (const Tout*)g, (const Tout*)b, (Tout*)out, copy_f32, H, eps);
+                       (const Tout*)g, (const Tout*)b, (Tout*)out, H, eps);
   else
     hipLaunchKernelGGL((norm_kernel<Tin, Tout, false>), dim3(rows), dim3(256), 0, s, (const Tin*)in,
-                       (const Tout*)g, (const Tout*)b, (Tout*)out, copy_f32, H, eps);
+                       (const Tout*)g, (const Tout*)b, (Tout*)out, H, eps);
 }
 
 hipError_t launch_norm(int dtype, bool in_f32, bool layer_norm, const void* in, const void* g,
-                       const void* b, void* out, float* copy_f32, int rows, int H, float eps,
-                       hipStream_t s) {
+                       const void* b, void* out, int rows, int H, float eps, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   if (dtype == 0)
-    norm_dispatch<float, float>(layer_norm, in, g, b, out, copy_f32, rows, H, eps, s);
+    norm_dispatch<float, float>(layer_norm, in, g, b, out, rows, H, eps, s);
   else if (in_f32)
-    norm_dispatch<float, bf16>(layer_norm, in, g, b, out, copy_f32, rows, H, eps, s);
+    norm_dispatch<float, bf16>(layer_norm, in, g, b, out, rows, H, eps, s);
   else
-    norm_dispatch<bf16, bf16>(layer_norm, in, g, b, out, copy_f32, rows, H, eps, s);
+    norm_dispatch<bf16, bf16>(layer_norm, in, g, b, out, rows, H, eps, s);
   return hipGetLastError();
 }
 
@@ -188,36 +181,57 @@ hipError_t launch_rope_append(int dtype, const RopeArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// ------------------------------------------------------------------ casts
-template <typename T>
-__global__ void cast_kernel(const float* __restrict__ in, T* __restrict__ out, size_t n) {
-  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
-    out[i] = from_f<T>(in[i]);
+// ------------------------------------------------------------------ split-K reduction
+// out = resid + parts[0] + parts[1] + ... (fixed order: deterministic).  Four
+// elements per thread when n is a multiple of 4, else one.
+template <typename Tr, typename To, int V>
+__global__ __launch_bounds__(256) void split_reduce_kernel(const Tr* __restrict__ resid, const float* __restrict__ parts,
+                                                           int n_split, size_t n, To* __restrict__ out) {
+  const size_t nv = n / V;
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < nv; i += (size_t)gridDim.x * blockDim.x) {
+    float acc[V];
+#pragma unroll
+    for (int e = 0; e < V; ++e) acc[e] = to_f<Tr>(resid[i * V + e]);
+    for (int sp = 0; sp < n_split; ++sp) {
+      const float* pp = parts + (size_t)sp * n + i * V;
+      if (V == 4) {
+        const float4 q = *reinterpret_cast<const float4*>(pp);
+        acc[0] += q.x; acc[1] += q.y; acc[2] += q.z; acc[V - 1] += q.w;
+      } else {
+#pragma unroll
+        for (int e = 0; e < V; ++e) acc[e] += pp[e];
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < V; ++e) out[i * V + e] = from_f<To>(acc[e]);
+  }
 }
 
-hipError_t launch_cast_out(int dtype, const float* acc, void* out, size_t n, hipStream_t s) {
-  if (n == 0) return hipSuccess;
-  const int blocks = (int)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096);
-  if (dtype == 0)
-    hipLaunchKernelGGL(cast_kernel<float>, dim3(blocks), dim3(256), 0, s, acc, (float*)out, n);
+template <typename Tr, typename To>
+static void split_reduce_dispatch(const void* resid, const float* parts, int n_split, size_t n, void* out,
+                                  hipStream_t s) {
+  const bool vec = (n % 4) == 0;
+  const size_t items = vec ? n / 4 : n;
+  const int blocks = (int)((items + 255) / 256 < 8192 ? (items + 255) / 256 : 8192);
+  if (vec)
+    hipLaunchKernelGGL((split_reduce_kernel<Tr, To, 4>), dim3(blocks), dim3(256), 0, s, (const Tr*)resid, parts,
+                       n_split, n, (To*)out);
   else
-    hipLaunchKernelGGL(cast_kernel<bf16>, dim3(blocks), dim3(256), 0, s, acc, (bf16*)out, n);
-  return hipGetLastError();
+    hipLaunchKernelGGL((split_reduce_kernel<Tr, To, 1>), dim3(blocks), dim3(256), 0, s, (const Tr*)resid, parts,
+                       n_split, n, (To*)out);
 }
 
-template <typename T>
-__global__ void to_f32_kernel(const T* __restrict__ in, float* __restrict__ out, size_t n) {
-  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
-    out[i] = to_f<T>(in[i]);
-}
-
-hipError_t launch_to_f32(int dtype, const void* in, float* out, size_t n, hipStream_t s) {
+hipError_t launch_split_reduce(int dtype, bool resid_f32, bool out_f32, const void* resid, const float* parts,
+                               int n_split, size_t n, void* out, hipStream_t s) {
   if (n == 0) return hipSuccess;
-  const int blocks = (int)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096);
-  if (dtype == 0)
-    hipLaunchKernelGGL(to_f32_kernel<float>, dim3(blocks), dim3(256), 0, s, (const float*)in, out, n);
+  if (dtype == 0 || (resid_f32 && out_f32))
+    split_reduce_dispatch<float, float>(resid, parts, n_split, n, out, s);
+  else if (resid_f32)
+    split_reduce_dispatch<float, bf16>(resid, parts, n_split, n, out, s);
+  else if (out_f32)
+    split_reduce_dispatch<bf16, float>(resid, parts, n_split, n, out, s);
   else
-    hipLaunchKernelGGL(to_f32_kernel<bf16>, dim3(blocks), dim3(256), 0, s, (const bf16*)in, out, n);
+    split_reduce_dispatch<bf16, bf16>(resid, parts, n_split, n, out, s);
   return hipGetLastError();
 }
 

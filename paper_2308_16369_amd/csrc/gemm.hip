@@ -6,9 +6,9 @@
 // chunks XOR-swizzled by row so the MFMA operand reads are bank-conflict
 // free).  Both operands are K-contiguous, so every lane reads 16 contiguous
 // bytes for either MFMA operand.  Epilogues fuse the residual add
-// (postproj, ffn_ln2), SiLU*mul (SwiGLU ffn_ln1) and GELU.  Split-K
-// accumulates fp32 partials atomically into a buffer that already holds the
-// residual.
+// (postproj, ffn_ln2), SiLU*mul (SwiGLU ffn_ln1) and GELU.  Split-K stores
+// one fp32 partial per split; a separate pass adds residual + partials in a
+// fixed order, so results do not depend on scheduling.
 //
 // fp32: a plain LDS-tiled FMA kernel with the same epilogues.
 #include "kernels.h"
@@ -16,7 +16,7 @@
 namespace sarathi {
 
 enum Epi { EPI_STORE = 0, EPI_GELU = 1, EPI_SWIGLU = 2, EPI_RESID_TO_F32 = 3, EPI_RESIDF32_TO_ACT = 4,
-           EPI_ATOMIC = 5 };
+           EPI_PARTIAL = 5 };
 
 struct GemmP {
   const void* A;        // [M, K]
@@ -24,13 +24,13 @@ struct GemmP {
   int M, N, K;          // N = output columns (SwiGLU: F)
   int k_split, n_split; // K elements per split; number of splits
   int tiles_m, tiles_n, n_tiles;
-  void* out;            // [M, N]: dtype, or fp32 for EPI_RESID_TO_F32 / EPI_ATOMIC
+  void* out;            // [M, N]: dtype, or fp32 for EPI_RESID_TO_F32; EPI_PARTIAL: fp32 [n_split][M, N]
   const void* resid;    // EPI_RESID_TO_F32: dtype [M,N]; EPI_RESIDF32_TO_ACT: fp32 [M,N]
 };
 
 // Output element handling shared by both kernels.
 template <typename T, int EPI>
-__device__ __forceinline__ void epi_store(const GemmP& p, int r, int c, float v) {
+__device__ __forceinline__ void epi_store(const GemmP& p, int r, int c, float v, int split = 0) {
   const size_t idx = (size_t)r * p.N + c;
   if (EPI == EPI_STORE) {
     reinterpret_cast<T*>(p.out)[idx] = from_f<T>(v);
@@ -40,8 +40,8 @@ __device__ __forceinline__ void epi_store(const GemmP& p, int r, int c, float v)
     reinterpret_cast<float*>(p.out)[idx] = to_f<T>(reinterpret_cast<const T*>(p.resid)[idx]) + v;
   } else if (EPI == EPI_RESIDF32_TO_ACT) {
     reinterpret_cast<T*>(p.out)[idx] = from_f<T>(reinterpret_cast<const float*>(p.resid)[idx] + v);
-  } else if (EPI == EPI_ATOMIC) {
-    unsafeAtomicAdd(reinterpret_cast<float*>(p.out) + idx, v);
+  } else if (EPI == EPI_PARTIAL) {
+    reinterpret_cast<float*>(p.out)[(size_t)split * p.M * p.N + idx] = v;
   }
 }
 
@@ -211,7 +211,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_kernel(GemmP p) {
 #pragma unroll
         for (int fn = 0; fn < FN; ++fn) {
           const int c = n0_out + wn * WTN + fn * 16 + (lane & 15);
-          if (c < p.N) epi_store<bf16, EPI>(p, r, c, acc[fm][fn][i]);
+          if (c < p.N) epi_store<bf16, EPI>(p, r, c, acc[fm][fn][i], split);
         }
       }
     }
@@ -317,7 +317,7 @@ static hipError_t run_bf16_epi(int epi, const GemmP& p, hipStream_t s) {
     case EPI_SWIGLU: return run_bf16<BM, BN, WGM, WGN, PD, EPI_SWIGLU>(p, s);
     case EPI_RESID_TO_F32: return run_bf16<BM, BN, WGM, WGN, PD, EPI_RESID_TO_F32>(p, s);
     case EPI_RESIDF32_TO_ACT: return run_bf16<BM, BN, WGM, WGN, PD, EPI_RESIDF32_TO_ACT>(p, s);
-    default: return run_bf16<BM, BN, WGM, WGN, PD, EPI_ATOMIC>(p, s);
+    default: return run_bf16<BM, BN, WGM, WGN, PD, EPI_PARTIAL>(p, s);
   }
 }
 
@@ -386,29 +386,26 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s) {
     case LIN_RESID: epi = EPI_RESID_TO_F32; break;
     default: epi = EPI_RESIDF32_TO_ACT; break;
   }
-  // Split-K for the residual ops when the tile grid leaves CUs idle: fp32
-  // partials are added atomically into an accumulator that starts out holding
-  // the residual (LIN_RESID: the fp32 output itself; LIN_RESID_F32IN: a.acc,
-  // cast to the output afterwards).  Each split covers whole groups of two
+  // Split-K for the residual ops when the tile grid leaves CUs idle: every
+  // split stores its fp32 partial, then one pass adds residual + partials in
+  // split order (deterministic).  Each split covers whole groups of two
   // 64-wide k-tiles.
   const int tiles = p.tiles_m * p.tiles_n;
   const bool resid_kind = a.kind == LIN_RESID || a.kind == LIN_RESID_F32IN;
-  const bool can_split = resid_kind && a.allow_split && (a.kind == LIN_RESID || a.acc != nullptr);
-  if (can_split && tiles < 256) {
+  int n_split = 1;
+  if (resid_kind && a.parts != nullptr && tiles < 256) {
     const int kgroups = (a.K + 127) / 128;
     int ns = (400 + tiles - 1) / tiles;
     if (ns > kgroups / 2) ns = kgroups / 2;
+    if (ns > MAX_SPLIT) ns = MAX_SPLIT;
+    if ((size_t)ns * a.M * a.N > a.parts_cap) ns = (int)(a.parts_cap / ((size_t)a.M * a.N));
     if (ns > 1) {
       const int g_per = (kgroups + ns - 1) / ns;
       p.k_split = g_per * 128;
       p.n_split = (a.K + p.k_split - 1) / p.k_split;
-      epi = EPI_ATOMIC;
-      float* accbuf = (a.kind == LIN_RESID) ? reinterpret_cast<float*>(a.out) : a.acc;
-      if (!a.acc_ready) {
-        hipError_t e = launch_to_f32(a.kind == LIN_RESID ? dtype : 0, a.resid, accbuf, (size_t)a.M * a.N, s);
-        if (e != hipSuccess) return e;
-      }
-      p.out = accbuf;
+      n_split = p.n_split;
+      epi = EPI_PARTIAL;
+      p.out = a.parts;
     }
   }
   p.n_tiles = p.tiles_m * p.tiles_n * p.n_split;
@@ -420,8 +417,9 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s) {
     default: e = run_bf16_epi<160, 128, 2, 2, 2>(epi, p, s); break;
   }
   if (e != hipSuccess) return e;
-  if (epi == EPI_ATOMIC && a.kind == LIN_RESID_F32IN)
-    return launch_cast_out(dtype, a.acc, a.out, (size_t)a.M * a.N, s);
+  if (n_split > 1)
+    return launch_split_reduce(dtype, a.kind == LIN_RESID_F32IN, a.kind == LIN_RESID, a.resid, a.parts, n_split,
+                               (size_t)a.M * a.N, a.out, s);
   return hipSuccess;
 }
 

@@ -19,10 +19,8 @@ struct MetaChunk {
 hipError_t launch_meta_write(const MetaChunk& chunk, int* dst, hipStream_t s);
 
 // ---- norms (one row per block).  in: [rows, H] of Tin; out: [rows, H] of dtype.
-// copy_f32 (optional): receives the input as fp32 (residual-stream init).
 hipError_t launch_norm(int dtype, bool in_f32, bool layer_norm, const void* in, const void* g,
-                       const void* b, void* out, float* copy_f32, int rows, int H, float eps,
-                       hipStream_t s);
+                       const void* b, void* out, int rows, int H, float eps, hipStream_t s);
 
 // ---- rotary embedding of q, k in place of the preproj output and K/V append.
 struct RopeArgs {
@@ -46,10 +44,10 @@ struct LinearArgs {
   const void* w;        // [N or 2N, K]
   const void* resid;    // LIN_RESID: dtype [M,N]; LIN_RESID_F32IN: fp32 [M,N]
   void* out;            // LIN_RESID: fp32 [M,N]; others dtype [M,N]
-  float* acc;           // LIN_RESID_F32IN: fp32 [M,N] split-K accumulator (null: no split-K)
-  bool allow_split;     // split-K permitted (LIN_RESID accumulates into out itself)
-  bool acc_ready;       // the accumulator already holds the residual as fp32
+  float* parts;         // residual kinds: fp32 scratch for split-K partials (null: no split-K)
+  size_t parts_cap;     // its capacity in floats
 };
+constexpr int MAX_SPLIT = 4;   // split-K partials: at most MAX_SPLIT x [M, N] fp32
 hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s);
 
 // ---- attention
@@ -94,9 +92,9 @@ struct CombineArgs {
 };
 hipError_t launch_attn_combine(int dtype, const CombineArgs& a, hipStream_t s);
 
-// fp32 accumulator -> dtype
-hipError_t launch_cast_out(int dtype, const float* acc, void* out, size_t n, hipStream_t s);
-// dtype (or fp32 when dtype == 0) -> fp32 copy
-hipError_t launch_to_f32(int dtype, const void* in, float* out, size_t n, hipStream_t s);
+// out[i] = resid[i] + sum_{s < n_split} parts[s * n + i], summed in split order
+// (resid: fp32 if resid_f32 else dtype; out: fp32 if out_f32 else dtype).
+hipError_t launch_split_reduce(int dtype, bool resid_f32, bool out_f32, const void* resid, const float* parts,
+                               int n_split, size_t n, void* out, hipStream_t s);
 
 }  // namespace sarathi

@@ -82,7 +82,7 @@ bool same_cfg(const sarathi_model_cfg* a, const sarathi_model_cfg* b) {
 }
 
 struct Layout {
-  size_t a, qkv, o, hres, m, yacc, part, meta, ping0, ping1, total;
+  size_t a, qkv, o, hres, m, parts, part, meta, ping0, ping1, total;
 };
 
 Layout make_layout(const sarathi_model_cfg* c, int T, int S) {
@@ -96,7 +96,7 @@ Layout make_layout(const sarathi_model_cfg* c, int T, int S) {
   L.o = take(T * QD * es);
   L.hres = take(T * H * 4);
   L.m = take(T * F * es);
-  L.yacc = take(T * H * 4);
+  L.parts = take((size_t)MAX_SPLIT * T * H * 4);
   const size_t max_pre = (size_t)((T + QBLOCK - 1) / QBLOCK) * ((S + PRE_SPLIT - 1) / PRE_SPLIT);
   const size_t max_dec = (size_t)T * ((S + SPLIT_KEYS - 1) / SPLIT_KEYS);
   L.part = take((max_pre * QBLOCK + max_dec) * c->n_heads * (c->head_dim + 2) * 4);
@@ -256,7 +256,8 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
   char* ws = c.ws;
   const int* meta = reinterpret_cast<const int*>(ws + c.L.meta);
   float* hres = reinterpret_cast<float*>(ws + c.L.hres);
-  float* yacc = reinterpret_cast<float*>(ws + c.L.yacc);
+  float* parts = reinterpret_cast<float*>(ws + c.L.parts);
+  const size_t parts_cap = (size_t)MAX_SPLIT * T * H;
   char* kv_layer = static_cast<char*>(c.kv->mem) + (size_t)layer * c.kv->st.layer * esize(cfg);
   hipError_t e;
   hipEvent_t* ev = prof_claim();
@@ -268,9 +269,9 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
     if (me != hipSuccess) return hip_fail(me, "stage event");   \
   } while (0)
 
-  // norm_1 (also leaves x in fp32 in hres, the split-K accumulator of postproj)
+  // norm_1
   SARATHI_MARK();
-  e = launch_norm(dt, false, ln, x_in, w->norm1_g, w->norm1_b, ws + c.L.a, hres, T, H, cfg->eps, c.s);
+  e = launch_norm(dt, false, ln, x_in, w->norm1_g, w->norm1_b, ws + c.L.a, T, H, cfg->eps, c.s);
   if (e != hipSuccess) return hip_fail(e, "norm_1");
 
   // preproj over all rows
@@ -290,7 +291,7 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
 
   // attention: the chunk and the decodes separately, then one combine pass
   SARATHI_MARK();
-  float* part = reinterpret_cast<float*>(ws + c.L.part);
+  float* part = reinterpret_cast<float*>(ws + c.L.part);   // attention partials
   if (P.n_pre > 0) {
     PrefillArgs pa{};
     pa.qkv = ws + c.L.qkv; pa.ld_qkv = 3 * QD; pa.kv_layer = kv_layer; pa.st = c.kv->st;
@@ -319,13 +320,13 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
   SARATHI_MARK();
   LinearArgs po{};
   po.kind = LIN_RESID; po.M = T; po.N = H; po.K = QD; po.x = ws + c.L.o; po.w = w->w_o; po.resid = x_in;
-  po.out = hres; po.allow_split = true; po.acc_ready = true;
+  po.out = hres; po.parts = parts; po.parts_cap = parts_cap;
   e = launch_linear(dt, po, c.s);
   if (e != hipSuccess) return hip_fail(e, "postproj");
 
-  // norm_2 (also copies hres into yacc, the split-K accumulator of ffn_ln2)
+  // norm_2
   SARATHI_MARK();
-  e = launch_norm(dt, true, ln, hres, w->norm2_g, w->norm2_b, ws + c.L.a, yacc, T, H, cfg->eps, c.s);
+  e = launch_norm(dt, true, ln, hres, w->norm2_g, w->norm2_b, ws + c.L.a, T, H, cfg->eps, c.s);
   if (e != hipSuccess) return hip_fail(e, "norm_2");
 
   // ffn_ln1 + activation
@@ -340,7 +341,7 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
   SARATHI_MARK();
   LinearArgs dn{};
   dn.kind = LIN_RESID_F32IN; dn.M = T; dn.N = H; dn.K = F; dn.x = ws + c.L.m; dn.w = w->w_down; dn.resid = hres;
-  dn.out = x_out; dn.acc = yacc; dn.allow_split = true; dn.acc_ready = true;
+  dn.out = x_out; dn.parts = parts; dn.parts_cap = parts_cap;
   e = launch_linear(dt, dn, c.s);
   if (e != hipSuccess) return hip_fail(e, "ffn_ln2");
   SARATHI_MARK();
@@ -445,7 +446,8 @@ int sarathi_workspace_layout(const sarathi_model_cfg* cfg, int n_tokens, int n_d
   if (n_tokens < 1 || n_decodes < 0 || n_decodes > n_tokens || max_seq_len < 1)
     return fail(SARATHI_EINVAL, "bad sizes");
   const Layout L = make_layout(cfg, n_tokens, max_seq_len);
-  out->a = L.a; out->qkv = L.qkv; out->o = L.o; out->hres = L.hres; out->m = L.m; out->total = L.total;
+  out->a = L.a; out->qkv = L.qkv; out->o = L.o; out->hres = L.hres; out->m = L.m;
+  out->ping[0] = L.ping0; out->ping[1] = L.ping1; out->total = L.total;
   return SARATHI_OK;
 }
 
@@ -525,7 +527,7 @@ int sarathi_profile_end(double* stage_ms, int* n_calls) {
 
 size_t sarathi_linear_scratch_bytes(int M, int N) {
   if (M < 1 || N < 1) return 0;
-  return (size_t)M * N * 4;
+  return (size_t)MAX_SPLIT * M * N * 4;
 }
 
 int sarathi_linear(int dtype, int kind, int M, int N, int K, const void* x, const void* w, const void* resid,
@@ -540,10 +542,10 @@ int sarathi_linear(int dtype, int kind, int M, int N, int K, const void* x, cons
   if (!aligned16(x) || !aligned16(w)) return fail(SARATHI_EINVAL, "x and w must be 16-byte aligned");
   LinearArgs a{};
   a.kind = kind; a.M = M; a.N = N; a.K = K; a.x = x; a.w = w; a.resid = resid; a.out = out;
-  a.allow_split = kind == SARATHI_LINEAR_RESID ||
-                  (kind == SARATHI_LINEAR_RESID_F32IN && scratch && scratch_bytes >= sarathi_linear_scratch_bytes(M, N));
-  a.acc = (kind == SARATHI_LINEAR_RESID_F32IN && a.allow_split) ? static_cast<float*>(scratch) : nullptr;
-  a.acc_ready = false;
+  if (needs_resid && scratch && aligned16(scratch)) {
+    a.parts = static_cast<float*>(scratch);
+    a.parts_cap = scratch_bytes / 4;
+  }
   hipError_t e = launch_linear(dtype, a, static_cast<hipStream_t>(hip_stream));
   if (e != hipSuccess) return hip_fail(e, "linear");
   return SARATHI_OK;

@@ -59,7 +59,8 @@ class sarathi_kv_strides(ct.Structure):
 
 
 class sarathi_ws_layout(ct.Structure):
-    _fields_ = [(n, ct.c_size_t) for n in ("a", "qkv", "o", "hres", "m", "total")]
+    _fields_ = [(n, ct.c_size_t) for n in ("a", "qkv", "o", "hres", "m")] + [("ping", ct.c_size_t * 2),
+                                                                             ("total", ct.c_size_t)]
 
 
 EXPORTS = {

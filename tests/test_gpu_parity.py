@@ -89,6 +89,37 @@ def test_linear_matches_oracle(dtype, kind, mnk):
     assert err <= TOL[dtype]
 
 
+@pytest.mark.parametrize("kind", [S.LINEAR_RESID, S.LINEAR_RESID_F32IN])
+def test_linear_split_k_deterministic(kind):
+    """Split-K (small M, large K) gives bit-identical results run to run, and
+    agrees with the unsplit op (no scratch) to fp32 summation order."""
+    M, N, K = 48, 5120, 13824
+    rng = np.random.default_rng(11 + kind)
+    x = wl.round_to_bf16(rng.standard_normal((M, K)).astype(np.float32))
+    w = wl.round_to_bf16((rng.standard_normal((N, K)) * 0.02).astype(np.float32))
+    resid = rng.standard_normal((M, N)).astype(np.float32)
+    if kind == S.LINEAR_RESID:
+        resid = wl.round_to_bf16(resid)
+    xd, wd = to_dev(x, "bf16"), to_dev(w, "bf16")
+    rd = to_dev(resid, "bf16") if kind == S.LINEAR_RESID else torch.from_numpy(resid).cuda()
+    odt = torch.float32 if kind == S.LINEAR_RESID else torch.bfloat16
+    scratch = torch.empty(S.sarathi_linear_scratch_bytes(M, N), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    outs = []
+    for use_scratch in (True, True, False):
+        out = torch.full((M, N), float("nan"), dtype=odt, device="cuda")
+        S.sarathi_linear(S.BF16, kind, M, N, K, xd.data_ptr(), wd.data_ptr(), rd.data_ptr(), out.data_ptr(),
+                         scratch.data_ptr() if use_scratch else 0, scratch.numel() if use_scratch else 0, stream)
+        outs.append(out)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits_of(outs[0]), bits_of(outs[1])), "split-K result differs between runs"
+    ref = resid.astype(np.float64) + oracle.linear(x, w)
+    for o in outs[0], outs[2]:
+        err = rel_err(from_dev(o), ref)
+        log(f"split-K kind {kind}: err {err:.3e}")
+        assert err <= TOL["bf16"]
+
+
 # ============================================================================ whole layer
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
