@@ -1,0 +1,282 @@
+"""Chunk-size ablation and tile-quantization sweep of the hybrid-batch layer.
+
+Effects of the chunk size the paper measures (Sec. 4.4, tile quantization;
+Sec. 5.4, ablation of chunked prefills), taken here on this library's kernels
+through the C-ABI:
+
+* tile quantization: the fused linear ops run whole output tiles over the
+  T = C + B rows of a batch, so the layer time rises in steps just past the
+  row-tile multiples (the paper's advice: choose the chunk so that chunk plus
+  piggybacked decodes fills whole tiles);
+* chunking overhead: a prompt of P tokens prefilled as P / c chunks of c
+  tokens costs more than one full prefill -- the matmuls are smaller and each
+  chunk re-reads the KV of every earlier chunk.  The overhead is reported for
+  the attention alone and for the whole layer, c from 64 to 512;
+* decode piggybacking: for a chunk of c tokens and B decodes, the decode time
+  per token of the hybrid batch (hybrid minus prefill-only time, over B)
+  against a decode-only batch (the accounting of Sec. 5.1.1).
+
+Inputs are seeded synthetic tensors drawn on the device (weights
+0.02 * N(0,1), activations and cached K/V N(0,1)); only timing is measured
+here -- the same kernels' results are checked against the oracle by the
+parity tests.
+
+Command line (one GPU):
+    python -m paper_2308_16369_amd.ablation --json out.json --md out.md
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import sys
+import time
+from dataclasses import dataclass
+from typing import Callable, Dict, List, Optional, Sequence, Tuple
+
+LINEAR_STAGES = ("preproj", "postproj", "ffn_ln1", "ffn_ln2")
+
+
+def chunk_plan(prompt_len: int, chunk: int) -> List[Tuple[int, int]]:
+    """(offset, length) of each chunk when a prompt of ``prompt_len`` tokens
+    is prefilled ``chunk`` tokens at a time (the last chunk may be shorter)."""
+    if prompt_len < 1 or chunk < 1:
+        raise ValueError("prompt_len and chunk must be positive")
+    return [(o, min(chunk, prompt_len - o)) for o in range(0, prompt_len, chunk)]
+
+
+def tile_lengths(lo: int, hi: int, step: int, tiles: Sequence[int]) -> List[int]:
+    """Row counts for the tile-quantization sweep: every ``step`` rows in
+    [lo, hi] plus each tile multiple m in range and m +- 1."""
+    pts = set(range(lo, hi + 1, step))
+    for t in tiles:
+        for m in range(t, hi + 2, t):
+            pts.update(v for v in (m - 1, m, m + 1) if lo <= v <= hi)
+    return sorted(pts)
+
+
+@dataclass
+class Batch:
+    prefill_slot: int
+    chunk_offset: int
+    chunk_len: int
+    decode_slots: List[int]
+    decode_ctx: List[int]
+
+    @property
+    def n_tokens(self) -> int:
+        return self.chunk_len + len(self.decode_slots)
+
+
+class LayerRunner:
+    """One layer on the device, a KV cache of ``n_slots`` x ``max_seq_len``
+    positions, and a workspace for up to ``max_tokens`` rows."""
+
+    def __init__(self, shape, n_slots: int, max_seq_len: int, max_tokens: int, max_decodes: int, seed: int = 0):
+        import torch
+
+        from workloads.stack import generate_layer_on_device
+        from . import sarathi as S
+
+        self.S, self.torch, self.shape = S, torch, shape
+        self.dev = generate_layer_on_device(shape, n_slots, max_seq_len, seed)
+        self.cfg = S.make_cfg(hidden=shape.hidden, n_heads=shape.n_heads, head_dim=shape.head_dim, ffn=shape.ffn,
+                              n_layers=1, norm=S.NORM_RMS if shape.norm == "rms" else S.NORM_LAYER,
+                              act=S.ACT_SWIGLU if shape.act == "swiglu" else S.ACT_GELU, rope=int(shape.rope),
+                              rope_base=shape.rope_base, eps=shape.eps,
+                              dtype=S.BF16 if shape.dtype == "bf16" else S.F32)
+        kvt = self.dev.kv
+        self.kv = S.sarathi_kv_alloc(self.cfg, n_slots, max_seq_len, kvt.data_ptr(),
+                                     kvt.numel() * kvt.element_size())
+        self.w = S.make_weights({k: t.data_ptr() for k, t in self.dev.weights.items()})
+        self.ws_bytes = S.sarathi_workspace_bytes(self.cfg, max_tokens, max_decodes, max_seq_len)
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device="cuda")
+        g = torch.Generator(device="cuda")
+        g.manual_seed(seed + 1)
+        self.x = torch.empty((max_tokens, shape.hidden), dtype=kvt.dtype, device="cuda").normal_(0.0, 1.0,
+                                                                                                generator=g)
+        self.y = torch.empty_like(self.x)
+        self.stream = torch.cuda.current_stream()
+
+    def call(self, b: Batch) -> Callable[[], None]:
+        """A zero-argument launcher of one layer call on batch ``b``."""
+        bb, keep = self.S.make_batch(b.prefill_slot, b.chunk_offset, b.chunk_len, list(b.decode_slots),
+                                     list(b.decode_ctx))
+        S, x, y = self.S, self.x, self.y
+
+        def launch(bb=bb, keep=keep):   # the closure keeps the host arrays alive
+            S.sarathi_hybrid_layer_forward(self.cfg, self.w, self.kv, 0, bb, x.data_ptr(), y.data_ptr(),
+                                           self.ws.data_ptr(), self.ws_bytes, self.stream.cuda_stream)
+        return launch
+
+    def time(self, calls: Sequence[Callable[[], None]], iters: int = 20, warmup: int = 3) -> float:
+        """Milliseconds for one pass over ``calls`` (launched back to back)."""
+        torch = self.torch
+        for _ in range(warmup):
+            for c in calls:
+                c()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(self.stream)
+        for _ in range(iters):
+            for c in calls:
+                c()
+        e1.record(self.stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / iters
+
+    def stages(self, calls: Sequence[Callable[[], None]], iters: int = 5) -> Dict[str, float]:
+        """Per-stage milliseconds summed over one pass of ``calls`` (HIP events
+        on the launch stream around each stage)."""
+        S, torch = self.S, self.torch
+        for c in calls:
+            c()
+        torch.cuda.synchronize()
+        S.sarathi_profile_begin(iters * len(calls))
+        for _ in range(iters):
+            for c in calls:
+                c()
+        torch.cuda.synchronize()
+        st, n = S.sarathi_profile_end()
+        return {k: v / iters for k, v in st.items()}
+
+
+def tile_quantization(r: LayerRunner, lengths: Sequence[int], iters: int = 20) -> List[dict]:
+    """Prefill-only layer calls of T rows (chunk at offset 0): total and
+    linear-op milliseconds per call, and microseconds per row."""
+    out = []
+    for T in lengths:
+        calls = [r.call(Batch(0, 0, T, [], []))]
+        ms = r.time(calls, iters)
+        st = r.stages(calls, 3)
+        lin = sum(st[k] for k in LINEAR_STAGES)
+        out.append({"rows": T, "ms": round(ms, 5), "linear_ms": round(lin, 5),
+                    "us_per_row": round(ms * 1e3 / T, 4),
+                    **{f"{k}_ms": round(st[k], 5) for k in LINEAR_STAGES}})
+    return out
+
+
+def chunking_overhead(r: LayerRunner, prompts: Sequence[int], chunks: Sequence[int], iters: int = 10) -> List[dict]:
+    """For each prompt length P and chunk size c: the time of the whole chunk
+    sequence (P / c prefill-only calls, each attending to every earlier
+    chunk) against one full prefill of P rows, for the attention stage and the
+    whole layer.  A chunk size of P is the full prefill itself."""
+    out = []
+    for P in prompts:
+        full_calls = [r.call(Batch(0, 0, P, [], []))]
+        full_ms = r.time(full_calls, iters)
+        full_attn = r.stages(full_calls, 3)["chunk_attention"]
+        for c in sorted(set(c for c in chunks if c < P) | {P}):
+            calls = [r.call(Batch(0, o, n, [], [])) for o, n in chunk_plan(P, c)]
+            ms = r.time(calls, iters)
+            st = r.stages(calls, 3)
+            out.append({"prompt": P, "chunk": c, "n_chunks": len(calls), "ms": round(ms, 4),
+                        "attn_ms": round(st["chunk_attention"], 4), "full_ms": round(full_ms, 4),
+                        "full_attn_ms": round(full_attn, 4), "overhead": round(ms / full_ms, 3),
+                        "attn_overhead": round(st["chunk_attention"] / full_attn, 3)})
+    return out
+
+
+def piggyback(r: LayerRunner, chunks: Sequence[int], decodes: Sequence[int], ctx: int, offset: int,
+              iters: int = 20) -> List[dict]:
+    """Hybrid batches of one chunk (c tokens at ``offset``) plus B decodes of
+    context ``ctx``: step time, decode time per token against a decode-only
+    batch of the same decodes (Sec. 5.1.1), and rows T = c + B."""
+    out = []
+    for c in chunks:
+        for B in decodes:
+            slots = list(range(1, B + 1))
+            ctxs = [ctx] * B
+            t_h = r.time([r.call(Batch(0, offset, c, slots, ctxs))], iters)
+            t_p = r.time([r.call(Batch(0, offset, c, [], []))], iters)
+            t_d = r.time([r.call(Batch(-1, 0, 0, slots, ctxs))], iters)
+            dec_h = (t_h - t_p) / B
+            dec_b = t_d / B
+            out.append({"chunk": c, "decodes": B, "rows": c + B, "hybrid_ms": round(t_h, 5),
+                        "prefill_only_ms": round(t_p, 5), "decode_only_ms": round(t_d, 5),
+                        "decode_us_per_token_hybrid": round(dec_h * 1e3, 3),
+                        "decode_us_per_token_decode_only": round(dec_b * 1e3, 3),
+                        "decode_speedup": round(dec_b / dec_h, 3) if dec_h > 0 else None})
+    return out
+
+
+def to_markdown(res: dict) -> str:
+    L = [f"# Chunk-size ablation and tile quantization: {res['workload']}", "",
+         f"Command: `{res['command']}`", "", "## Tile quantization (prefill-only layer call of T rows)", "",
+         "| T | layer ms | linear ms | us/row | preproj | postproj | ffn_ln1 | ffn_ln2 |",
+         "|---|---|---|---|---|---|---|---|"]
+    for e in res["tile_quantization"]:
+        L.append(f"| {e['rows']} | {e['ms']:.4f} | {e['linear_ms']:.4f} | {e['us_per_row']:.3f} | "
+                 f"{e['preproj_ms']:.4f} | {e['postproj_ms']:.4f} | {e['ffn_ln1_ms']:.4f} | {e['ffn_ln2_ms']:.4f} |")
+    L += ["", "## Chunked prefill against one full prefill (Sec. 5.4)", "",
+          "| prompt | chunk | chunks | layer ms | overhead | attention ms | attention overhead |",
+          "|---|---|---|---|---|---|---|"]
+    for e in res["chunking_overhead"]:
+        L.append(f"| {e['prompt']} | {e['chunk']} | {e['n_chunks']} | {e['ms']:.3f} | {e['overhead']:.3f} | "
+                 f"{e['attn_ms']:.3f} | {e['attn_overhead']:.3f} |")
+    L += ["", f"## Decode piggybacking (decodes of context {res['piggyback_ctx']}, chunk at offset "
+              f"{res['piggyback_offset']})", "",
+          "| chunk | decodes | T | hybrid ms | prefill-only ms | decode-only ms | decode us/token hybrid | "
+          "decode-only | speedup |", "|---|---|---|---|---|---|---|---|---|"]
+    for e in res["piggyback"]:
+        L.append(f"| {e['chunk']} | {e['decodes']} | {e['rows']} | {e['hybrid_ms']:.4f} | {e['prefill_only_ms']:.4f} | "
+                 f"{e['decode_only_ms']:.4f} | {e['decode_us_per_token_hybrid']:.2f} | "
+                 f"{e['decode_us_per_token_decode_only']:.2f} | {e['decode_speedup']} |")
+    return "\n".join(L) + "\n"
+
+
+def main(argv: Optional[Sequence[str]] = None) -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--workload", default="llama13b", choices=["llama13b", "tiny"])
+    ap.add_argument("--json", default=None)
+    ap.add_argument("--md", default=None)
+    ap.add_argument("--quick", action="store_true", help="a few points of each sweep")
+    args = ap.parse_args(argv)
+
+    import torch
+
+    import workloads as wl
+
+    assert torch.cuda.is_available(), "the ablation runs on a GPU"
+    if args.workload == "llama13b":
+        shape = wl.LLAMA13B_LAYER.shape
+        prompts = [1024, 2048] if args.quick else [1024, 2048, 3072]
+        chunks = [64, 128, 256, 512]
+        lengths = [128, 129, 256, 257] if args.quick else tile_lengths(32, 512, 32, [64, 96, 128, 160])
+        pig_chunks = [128, 256] if args.quick else [64, 128, 192, 256, 320, 384, 512]
+        pig_dec = [32, 64] if args.quick else [16, 32, 63, 64, 96, 128]
+        ctx, offset = 1024, 1024
+    else:
+        shape = wl.with_dtype(wl.TINY, "bf16").shape
+        prompts, chunks = [256], [64, 128]
+        lengths = [64, 65, 128]
+        pig_chunks, pig_dec = [64], [4]
+        ctx, offset = 100, 64
+    max_seq = max(max(prompts), ctx + 2, offset + max(pig_chunks))
+    n_slots = 1 + max(pig_dec)
+    max_tokens = max(max(prompts), max(lengths), max(pig_chunks) + max(pig_dec))
+    t0 = time.time()
+    r = LayerRunner(shape, n_slots, max_seq, max_tokens, max(pig_dec))
+    log = lambda m: print(f"# {m} ({time.time() - t0:.1f}s)", file=sys.stderr, flush=True)
+    log("inputs on the device")
+    res = {"workload": f"{args.workload}-layer-{shape.dtype}", "command":
+           "python -m paper_2308_16369_amd.ablation " + " ".join(argv if argv is not None else sys.argv[1:])}
+    res["tile_quantization"] = tile_quantization(r, lengths)
+    log("tile quantization done")
+    res["chunking_overhead"] = chunking_overhead(r, prompts, chunks)
+    log("chunking overhead done")
+    res["piggyback_ctx"], res["piggyback_offset"] = ctx, offset
+    res["piggyback"] = piggyback(r, pig_chunks, pig_dec, ctx, offset)
+    log("piggyback done")
+    if args.json:
+        with open(args.json, "w") as f:
+            json.dump(res, f, indent=1)
+    if args.md:
+        with open(args.md, "w") as f:
+            f.write(to_markdown(res))
+    print(json.dumps({"workload": res["workload"], "points": {k: len(v) for k, v in res.items()
+                                                             if isinstance(v, list)}}))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -171,6 +171,18 @@ def test_layer_head_dim_128_tiny_bf16():
     run_and_check(wl.make_instance(shape, b, max_seq_len=512, n_slots=4, seed=5), "hd128 tiny bf16")
 
 
+@pytest.mark.parametrize("C,off,decodes", [(2048, 0, []), (1000, 2048, [(0, 3047), (2, 17)])])
+def test_layer_long_chunk_bf16(C, off, decodes):
+    """Chunks as long as the full prefills of the chunk-size ablation (a
+    2048-token prompt in one call; a 1000-row chunk after 2048 cached
+    positions with decodes beside it), head_dim 128."""
+    shape = _tiny_shape("bf16", hidden=512, n_heads=4, head_dim=128, ffn=1376)
+    b = wl.Batch(prefill_slot=1, chunk_offset=off, chunk_len=C,
+                 decode_slots=np.array([d[0] for d in decodes], np.int32),
+                 decode_ctx=np.array([d[1] for d in decodes], np.int32))
+    run_and_check(wl.make_instance(shape, b, max_seq_len=3072, n_slots=3, seed=41), f"long chunk {C}@{off}")
+
+
 # ============================================================================ method invariants on the GPU
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])

@@ -69,3 +69,35 @@ def generate_stack_on_device(w: Workload) -> DeviceStack:
             lw["norm2_b"] = torch.empty(H, dtype=bf, device="cuda").normal_(0.0, 0.02, generator=g)
         weights.append(lw)
     return DeviceStack(workload=w, batch=batch, x=x, kv=kv, weights=weights)
+
+
+@dataclass
+class DeviceLayer:
+    """One layer's weights and a KV cache on the device (for timing sweeps)."""
+    shape: "object"
+    kv: "object"                 # torch [1, n_slots, 2, nh, S, d]
+    weights: dict
+
+
+def generate_layer_on_device(shp, n_slots: int, max_seq_len: int, seed: int = 0) -> DeviceLayer:
+    """Weights of one layer plus a KV cache whose every position holds a
+    finite N(0,1) value (timing sweeps read prefixes written by nobody)."""
+    import torch
+
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    dt = torch.bfloat16 if shp.dtype == "bf16" else torch.float32
+    H, nh, d, F = shp.hidden, shp.n_heads, shp.head_dim, shp.ffn
+    kv = torch.empty((1, n_slots, 2, nh, max_seq_len, d), dtype=dt, device="cuda").normal_(0.0, 1.0, generator=g)
+    lw = {
+        "w_qkv": torch.empty((3 * nh * d, H), dtype=dt, device="cuda").normal_(0.0, 0.02, generator=g),
+        "w_o": torch.empty((H, nh * d), dtype=dt, device="cuda").normal_(0.0, 0.02, generator=g),
+        "w_up": torch.empty((shp.up_rows, H), dtype=dt, device="cuda").normal_(0.0, 0.02, generator=g),
+        "w_down": torch.empty((H, F), dtype=dt, device="cuda").normal_(0.0, 0.02, generator=g),
+        "norm1_g": torch.empty(H, dtype=dt, device="cuda").normal_(1.0, 0.02, generator=g),
+        "norm2_g": torch.empty(H, dtype=dt, device="cuda").normal_(1.0, 0.02, generator=g),
+    }
+    if shp.norm == "layer":
+        lw["norm1_b"] = torch.empty(H, dtype=dt, device="cuda").normal_(0.0, 0.02, generator=g)
+        lw["norm2_b"] = torch.empty(H, dtype=dt, device="cuda").normal_(0.0, 0.02, generator=g)
+    return DeviceLayer(shape=shp, kv=kv, weights=lw)
