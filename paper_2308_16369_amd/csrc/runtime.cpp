@@ -13,6 +13,7 @@
 #include <string>
 #include <vector>
 
+#include "host_error.h"
 #include "kernels.h"
 #include "sarathi.h"
 
@@ -28,11 +29,10 @@ struct sarathi_kv {
 };
 
 namespace {
-
 thread_local std::string g_err;
+}  // namespace
 
-int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
-int fail(int code, const char* fmt, ...) {
+int sarathi::fail(int code, const char* fmt, ...) {
   char buf[512];
   va_list ap;
   va_start(ap, fmt);
@@ -41,6 +41,8 @@ int fail(int code, const char* fmt, ...) {
   g_err = buf;
   return code;
 }
+
+namespace {
 
 int hip_fail(hipError_t e, const char* what) {
   return fail(SARATHI_EHIP, "%s: %s", what, hipGetErrorString(e));

@@ -23,6 +23,7 @@ F32, BF16 = 0, 1
 NORM_RMS, NORM_LAYER = 0, 1
 ACT_SWIGLU, ACT_GELU = 0, 1
 LINEAR_PLAIN, LINEAR_RESID, LINEAR_RESID_F32IN, LINEAR_SWIGLU, LINEAR_GELU = 0, 1, 2, 3, 4
+POLICY_DECODE_MAXIMAL, POLICY_PREFILL_DECODE, POLICY_MIXED = 0, 1, 2
 
 _ERRNAMES = {EINVAL: "EINVAL", ERANGE: "ERANGE", ENOSPC: "ENOSPC", EUNSUPPORTED: "EUNSUPPORTED", EHIP: "EHIP"}
 
@@ -63,6 +64,24 @@ class sarathi_ws_layout(ct.Structure):
                                                                              ("total", ct.c_size_t)]
 
 
+class sarathi_sched_cfg(ct.Structure):
+    _fields_ = [(n, ct.c_int) for n in ("policy", "max_batch", "chunk", "max_chunks", "max_tokens", "n_slots",
+                                        "max_seq_len")]
+
+
+class sarathi_sched_step(ct.Structure):
+    _fields_ = [("n_tokens", ct.c_int), ("n_chunks", ct.c_int)] + \
+        [(n, ct.POINTER(ct.c_int)) for n in ("chunk_request", "chunk_slot", "chunk_offset", "chunk_len")] + \
+        [("n_decodes", ct.c_int)] + \
+        [(n, ct.POINTER(ct.c_int)) for n in ("decode_request", "decode_slot", "decode_ctx")]
+
+
+class sarathi_sched_stats(ct.Structure):
+    _fields_ = [(n, ct.c_longlong) for n in ("iterations", "prefill_tokens", "decode_tokens", "hybrid_iterations",
+                                             "prefill_only_iterations", "decode_only_iterations")] + \
+        [(n, ct.c_int) for n in ("submitted", "admitted", "finished", "resident")]
+
+
 EXPORTS = {
     "sarathi_version": (ct.c_int, []),
     "sarathi_last_error": (ct.c_char_p, []),
@@ -85,6 +104,12 @@ EXPORTS = {
     "sarathi_linear_scratch_bytes": (ct.c_size_t, [ct.c_int, ct.c_int]),
     "sarathi_linear": (ct.c_int, [ct.c_int, ct.c_int, ct.c_int, ct.c_int, ct.c_int, ct.c_void_p, ct.c_void_p,
                                   ct.c_void_p, ct.c_void_p, ct.c_void_p, ct.c_size_t, ct.c_void_p]),
+    "sarathi_sched_create": (ct.c_int, [ct.POINTER(sarathi_sched_cfg), ct.POINTER(ct.c_void_p)]),
+    "sarathi_sched_destroy": (None, [ct.c_void_p]),
+    "sarathi_sched_submit": (ct.c_int, [ct.c_void_p, ct.c_int, ct.c_int, ct.POINTER(ct.c_int)]),
+    "sarathi_sched_next": (ct.c_int, [ct.c_void_p, ct.POINTER(sarathi_sched_step)]),
+    "sarathi_sched_commit": (ct.c_int, [ct.c_void_p]),
+    "sarathi_sched_get_stats": (ct.c_int, [ct.c_void_p, ct.POINTER(sarathi_sched_stats)]),
 }
 
 _lib: Optional[ct.CDLL] = None
@@ -231,3 +256,78 @@ def sarathi_linear(dtype, kind, M, N, K, x: int, w: int, resid: int, out: int, s
     rc = lib().sarathi_linear(dtype, kind, M, N, K, ct.c_void_p(x), ct.c_void_p(w), ct.c_void_p(resid or None),
                               ct.c_void_p(out), ct.c_void_p(scratch or None), scratch_bytes, ct.c_void_p(stream))
     return _check(rc) if check else rc
+
+
+# ---------------------------------------------------------------------------- scheduler
+
+class Step:
+    """One iteration described by the scheduler (copied out of its arrays)."""
+
+    def __init__(self, st: sarathi_sched_step):
+        def arr(p, n):
+            return [p[i] for i in range(n)]
+        self.n_tokens = st.n_tokens
+        self.chunk_request = arr(st.chunk_request, st.n_chunks)
+        self.chunk_slot = arr(st.chunk_slot, st.n_chunks)
+        self.chunk_offset = arr(st.chunk_offset, st.n_chunks)
+        self.chunk_len = arr(st.chunk_len, st.n_chunks)
+        self.decode_request = arr(st.decode_request, st.n_decodes)
+        self.decode_slot = arr(st.decode_slot, st.n_decodes)
+        self.decode_ctx = arr(st.decode_ctx, st.n_decodes)
+
+    @property
+    def n_chunks(self) -> int:
+        return len(self.chunk_len)
+
+    @property
+    def n_decodes(self) -> int:
+        return len(self.decode_ctx)
+
+    def hybrid_batch(self):
+        """(sarathi_hybrid_batch, keepalive) for an iteration of at most one chunk."""
+        if self.n_chunks > 1:
+            raise ValueError("an iteration with several chunks needs the mixed-batch entry points")
+        if self.n_chunks == 1:
+            return make_batch(self.chunk_slot[0], self.chunk_offset[0], self.chunk_len[0], self.decode_slot,
+                              self.decode_ctx)
+        return make_batch(-1, 0, 0, self.decode_slot, self.decode_ctx)
+
+
+class Scheduler:
+    """Owner of one sarathi_sched (include/sarathi_sched.h)."""
+
+    def __init__(self, policy: int, max_batch: int, n_slots: int, max_seq_len: int, chunk: int = 0,
+                 max_chunks: int = 0, max_tokens: int = 0):
+        cfg = sarathi_sched_cfg(policy, max_batch, chunk, max_chunks, max_tokens, n_slots, max_seq_len)
+        h = ct.c_void_p()
+        _check(lib().sarathi_sched_create(ct.byref(cfg), ct.byref(h)))
+        self._h = h
+
+    def close(self):
+        if self._h:
+            lib().sarathi_sched_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def submit(self, prompt_len: int, decode_len: int) -> int:
+        rid = ct.c_int()
+        _check(lib().sarathi_sched_submit(self._h, prompt_len, decode_len, ct.byref(rid)))
+        return rid.value
+
+    def next(self) -> Step:
+        st = sarathi_sched_step()
+        _check(lib().sarathi_sched_next(self._h, ct.byref(st)))
+        return Step(st)
+
+    def commit(self):
+        _check(lib().sarathi_sched_commit(self._h))
+
+    def stats(self) -> dict:
+        st = sarathi_sched_stats()
+        _check(lib().sarathi_sched_get_stats(self._h, ct.byref(st)))
+        return {n: getattr(st, n) for n, _ in sarathi_sched_stats._fields_}
