@@ -127,8 +127,15 @@ def stage_work(shp, b, S_stats=None):
     w["norm_1"] = (0.0, 2 * T * H * es + T * H * 4)
     w["preproj"] = (2.0 * T * H * 3 * QD, 3 * QD * H * es + T * H * es + T * 3 * QD * es)
     w["rope_kv_append"] = (0.0, 2 * T * 3 * QD * es + T * QD * es)
-    w["chunk_attention"] = (4.0 * pre_pairs * hd * nh, pre_keys * 2 * QD * es + 2 * C * QD * es)
-    w["decode_attention"] = (4.0 * dec_keys * hd * nh, dec_keys * 2 * QD * es + 2 * B * QD * es)
+    # key-split partials (hd + 2 fp32 per head): decode rows split every 256
+    # keys; chunk rows in 64-row query blocks split every 256 keys (the
+    # runtime's work decomposition)
+    dec_parts = sum(-(-(c + 1) // 256) for c in ctx)
+    pre_parts = sum(64 * -(-(b.chunk_offset + min((qb + 1) * 64, C)) // 256) for qb in range(-(-C // 64)))
+    part_bytes = nh * (hd + 2) * 4
+    w["chunk_attention"] = (4.0 * pre_pairs * hd * nh, pre_keys * 2 * QD * es + C * QD * es + pre_parts * part_bytes)
+    w["decode_attention"] = (4.0 * dec_keys * hd * nh, dec_keys * 2 * QD * es + B * QD * es + dec_parts * part_bytes)
+    w["attention_combine"] = (0.0, (dec_parts + pre_parts) * part_bytes + T * QD * es)
     w["postproj"] = (2.0 * T * QD * H, H * QD * es + T * QD * es + T * H * es + T * H * 4)
     w["norm_2"] = (0.0, T * H * 4 + T * H * es + T * H * 4)
     w["ffn_ln1"] = (2.0 * T * H * up_rows, up_rows * H * es + T * H * es + T * F * es)
@@ -154,7 +161,8 @@ def counter_traffic(stage: str, workload: str):
 
 
 BOUND = {"norm_1": "hbm", "preproj": "mfma", "rope_kv_append": "hbm", "chunk_attention": "mfma",
-         "decode_attention": "hbm", "postproj": "mfma", "norm_2": "hbm", "ffn_ln1": "mfma", "ffn_ln2": "mfma"}
+         "decode_attention": "hbm", "attention_combine": "hbm", "postproj": "mfma", "norm_2": "hbm",
+         "ffn_ln1": "mfma", "ffn_ln2": "mfma"}
 
 
 def main():

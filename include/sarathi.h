@@ -248,18 +248,18 @@ int sarathi_linear(int dtype, int kind, int M, int N, int K, const void* x, cons
  * Measurement hook: between sarathi_profile_begin and sarathi_profile_end,
  * every layer call (also each layer of sarathi_model_step) records a HIP
  * event on its stream before each of the SARATHI_N_STAGES stages and after
- * the last, from a host-side pool of 10 * max_calls events (no device
- * memory).  Calls beyond max_calls are not recorded.
+ * the last, from a host-side pool of (SARATHI_N_STAGES + 1) * max_calls
+ * events (no device memory).  Calls beyond max_calls are not recorded.
  * sarathi_profile_end waits for the last recorded event, writes the summed
  * elapsed milliseconds of each stage over all recorded calls into
  * stage_ms[SARATHI_N_STAGES] and the number of recorded layer calls into
  * *n_calls, and stops recording.  Errors: EINVAL (bad max_calls, end without
  * begin, NULL outputs), EHIP.
  * Stages: 0 norm_1, 1 preproj, 2 rotary embedding + KV append, 3 chunk
- * attention, 4 decode attention (incl. split combine), 5 postproj, 6 norm_2,
- * 7 ffn_ln1, 8 ffn_ln2.
+ * attention, 4 decode attention, 5 combine of the attention key-splits,
+ * 6 postproj, 7 norm_2, 8 ffn_ln1, 9 ffn_ln2.
  */
-#define SARATHI_N_STAGES 9
+#define SARATHI_N_STAGES 10
 int sarathi_profile_begin(int max_calls);
 int sarathi_profile_end(double* stage_ms, int* n_calls);
 

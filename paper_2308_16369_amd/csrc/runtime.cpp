@@ -312,6 +312,7 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
     e = launch_attn_rows(dt, da, c.s);
     if (e != hipSuccess) return hip_fail(e, "decode attention");
   }
+  SARATHI_MARK();
   CombineArgs ca{};
   ca.part = part; ca.comb = meta + P.o_comb; ca.n_rows = T; ca.nh = nh; ca.hd = hd; ca.out = ws + c.L.o;
   ca.ld_out = QD;

@@ -230,8 +230,9 @@ def sarathi_model_step(cfg, weights: Sequence[sarathi_layer_weights], kv: KV, ba
     return _check(rc) if check else rc
 
 
-N_STAGES = 9
-STAGE_NAMES = ["norm_1", "preproj", "rope_kv_append", "chunk_attention", "decode_attention", "postproj", "norm_2",
+N_STAGES = 10
+STAGE_NAMES = ["norm_1", "preproj", "rope_kv_append", "chunk_attention", "decode_attention", "attention_combine",
+               "postproj", "norm_2",
                "ffn_ln1", "ffn_ln2"]
 
 
