@@ -119,6 +119,27 @@ typedef struct {
   const int* decode_ctx_lens;
 } sarathi_hybrid_batch;
 
+/*
+ * Mixed batch: any number of prompt chunks plus decodes (the iteration-level
+ * batching of Orca, which Sec. 5.2 compares against; with n_chunks <= 1 it
+ * is the hybrid batch above).  Host memory.
+ *   chunk i: chunk_lens[i] >= 1 tokens of the request in slot chunk_slots[i]
+ *            at positions chunk_offsets[i] .. + chunk_lens[i] - 1 (earlier
+ *            positions of that slot already cached);
+ *   decodes: as in sarathi_hybrid_batch.
+ * Rows of x_in / x_out: chunk 0's rows in position order, then chunk 1's, ...,
+ * then the decodes in array order.  All slots distinct.
+ */
+typedef struct {
+  int        n_chunks;
+  const int* chunk_slots;
+  const int* chunk_offsets;
+  const int* chunk_lens;
+  int        n_decodes;
+  const int* decode_slots;
+  const int* decode_ctx_lens;
+} sarathi_mixed_batch;
+
 /* ------------------------------------------------------------------ KV cache */
 /*
  * Pre-allocated per-request KV slabs (Sec. 4.5), laid out
@@ -176,6 +197,12 @@ size_t sarathi_workspace_bytes(const sarathi_model_cfg* cfg, int max_tokens, int
                                int max_seq_len);
 int sarathi_workspace_layout(const sarathi_model_cfg* cfg, int n_tokens, int n_decodes,
                              int max_seq_len, sarathi_ws_layout* out);
+/* The same for mixed batches of up to max_chunks (n_chunks) prompt chunks;
+ * with one chunk these equal the functions above. */
+size_t sarathi_mixed_workspace_bytes(const sarathi_model_cfg* cfg, int max_tokens, int max_chunks,
+                                     int max_seq_len);
+int sarathi_mixed_workspace_layout(const sarathi_model_cfg* cfg, int n_tokens, int n_chunks,
+                                   int max_seq_len, sarathi_ws_layout* out);
 
 /* ------------------------------------------------------------------ forward */
 /*
@@ -215,6 +242,24 @@ int sarathi_model_step(const sarathi_model_cfg* cfg, const sarathi_layer_weights
                        sarathi_kv* kv, const sarathi_hybrid_batch* batch,
                        const void* x_in, void* x_out, void* ws, size_t ws_bytes,
                        void* hip_stream);
+
+/*
+ * sarathi_hybrid_layer_forward / sarathi_model_step over a mixed batch (any
+ * number of prompt chunks, Sec. 5.2's mixed batching): the linear ops run
+ * over all rows, each chunk's attention over its own slot, each decode over
+ * its slot.  Same contract; the workspace is sized by
+ * sarathi_mixed_workspace_layout for this batch's rows and chunk count.
+ * Extra errors: EINVAL (n_chunks < 0 or > 65536, NULL chunk arrays), ERANGE
+ * (a chunk length < 1).
+ */
+int sarathi_mixed_layer_forward(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w,
+                                sarathi_kv* kv, int layer, const sarathi_mixed_batch* batch,
+                                const void* x_in, void* x_out, void* ws, size_t ws_bytes,
+                                void* hip_stream);
+int sarathi_mixed_model_step(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w,
+                             sarathi_kv* kv, const sarathi_mixed_batch* batch,
+                             const void* x_in, void* x_out, void* ws, size_t ws_bytes,
+                             void* hip_stream);
 
 /* ------------------------------------------------------------------ building block */
 /*

@@ -18,6 +18,6 @@ paper; beyond those pins they are pinned only through the invariants
 (chunking, batch and concatenation invariance, residual identity).
 """
 from .layer import (  # noqa: F401
-    OracleBatch, LayerOut, rms_norm, layer_norm, linear, rope_rotate, silu, gelu,
+    OracleBatch, OracleMixedBatch, LayerOut, rms_norm, layer_norm, linear, rope_rotate, silu, gelu,
     attend, layer_forward, model_step, token_positions, chunk_visibility,
 )

@@ -44,6 +44,21 @@ class OracleBatch:
 
 
 @dataclass
+class OracleMixedBatch:
+    """Batch of several prompt chunks plus decodes (the iteration-level mixed
+    batching that Sec. 5.2 compares against; the hybrid batch is the case of
+    at most one chunk).  chunks: [(slot, offset, length)]; rows are chunk 0
+    in position order, chunk 1, ..., then the decodes."""
+    chunks: Sequence[Sequence[int]]
+    decode_slots: Sequence[int]
+    decode_ctx: Sequence[int]
+
+    @property
+    def n_tokens(self) -> int:
+        return sum(int(c[2]) for c in self.chunks) + len(self.decode_slots)
+
+
+@dataclass
 class LayerOut:
     y: np.ndarray          # [T, H] layer output
     q: np.ndarray          # [T, nh, d] queries after rotation
@@ -139,13 +154,21 @@ def attend(q: np.ndarray, keys: np.ndarray, values: np.ndarray) -> np.ndarray:
     return np.einsum("hn,hnd->hd", w, values)
 
 
-def token_positions(batch: OracleBatch):
-    """(slot, position) of every row of the hybrid batch: chunk rows at
-    offset..offset+C-1 of the prefill slot, then each decode at its context
-    length [Sec. 4.2 chunk offsets; Sec. 4.3 row concatenation]."""
-    C = batch.chunk_len
-    slots = [batch.prefill_slot] * C + [int(s) for s in batch.decode_slots]
-    pos = [batch.chunk_offset + r for r in range(C)] + [int(c) for c in batch.decode_ctx]
+def token_positions(batch):
+    """(slot, position) of every row of the batch: chunk rows at
+    offset..offset+C-1 of their slot, then each decode at its context length
+    [Sec. 4.2 chunk offsets; Sec. 4.3 row concatenation].  ``batch`` is an
+    OracleBatch or an OracleMixedBatch."""
+    if isinstance(batch, OracleMixedBatch):
+        chunks = [(int(s), int(o), int(n)) for s, o, n in batch.chunks]
+    else:
+        chunks = [(batch.prefill_slot, batch.chunk_offset, batch.chunk_len)] if batch.chunk_len else []
+    slots, pos = [], []
+    for s, o, n in chunks:
+        slots += [s] * n
+        pos += [o + r for r in range(n)]
+    slots += [int(s) for s in batch.decode_slots]
+    pos += [int(c) for c in batch.decode_ctx]
     return np.asarray(slots, dtype=np.int64), np.asarray(pos, dtype=np.int64)
 
 

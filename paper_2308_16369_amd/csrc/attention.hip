@@ -59,29 +59,31 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(PrefillArgs a, f
   __shared__ u32x4 vs_[2][KT * DCH];     // V tile [key][D], chunk ^ (key & 7)
 
   const int item = blockIdx.x, h = blockIdx.y;
-  const int wv = a.work[item];
+  const int* ch = a.chunks + 4 * a.work[2 * item];
+  const int slot = ch[0], offset = ch[1], C = ch[2], row0 = ch[3];
+  const int wv = a.work[2 * item + 1];
   const int q0 = (wv >> 12) * 64, ksplit = wv & 4095;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int grp = lane >> 4, ql = lane & 15;
-  const bf16* qkv = reinterpret_cast<const bf16*>(a.qkv);
+  const bf16* qkv = reinterpret_cast<const bf16*>(a.qkv) + (size_t)row0 * a.ld_qkv;
   const bf16* cache = reinterpret_cast<const bf16*>(a.kv_layer);
-  const bf16* kbase = cache + (size_t)a.slot * a.st.slot + (size_t)h * a.st.head;
+  const bf16* kbase = cache + (size_t)slot * a.st.slot + (size_t)h * a.st.head;
   const bf16* vbase = kbase + a.st.kv;
 
   // This item's keys: [kbeg, kend) within 0 .. off + min(q0 + 64, C) - 1.
-  const int n_keys = a.offset + min(q0 + 64, a.C);
+  const int n_keys = offset + min(q0 + 64, C);
   const int kbeg = ksplit * a.split_keys;
   const int kend = min(n_keys, kbeg + a.split_keys);
   const int n_tiles = (kend - kbeg + KT - 1) / KT;
 
   // The lane's query (B operand of S^T): q = ql, d = ks*32 + 8*grp.
   const int myq = q0 + wave * 16 + ql;
-  const int qpos = a.offset + myq;
+  const int qpos = offset + myq;
   u32x4 qf[D / 32];
 #pragma unroll
   for (int ks = 0; ks < D / 32; ++ks) {
-    const u32x4 v = *reinterpret_cast<const u32x4*>(qkv + (size_t)min(myq, a.C - 1) * a.ld_qkv + h * D + ks * 32 + 8 * grp);
-    qf[ks] = (myq < a.C) ? v : u32x4{0u, 0u, 0u, 0u};
+    const u32x4 v = *reinterpret_cast<const u32x4*>(qkv + (size_t)min(myq, C - 1) * a.ld_qkv + h * D + ks * 32 + 8 * grp);
+    qf[ks] = (myq < C) ? v : u32x4{0u, 0u, 0u, 0u};
   }
 
   float m_run = -INFINITY, l_run = 0.f;
@@ -204,7 +206,7 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(PrefillArgs a, f
 
   // ---- partial of the lane's query (rows < C): [m, l, o[D]].
   const int rb = wave * 16 + ql;
-  if (q0 + rb < a.C) {
+  if (q0 + rb < C) {
     float* dst = a.part + ((size_t)(item * 64 + rb) * a.nh + h) * (D + 2);
     if (grp == 0) {
       dst[0] = m_run;
@@ -218,7 +220,7 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(PrefillArgs a, f
 }
 
 hipError_t launch_attn_prefill(int dtype, const PrefillArgs& a, hipStream_t s) {
-  if (a.C <= 0 || a.n_work <= 0) return hipSuccess;
+  if (a.n_work <= 0) return hipSuccess;
   if (dtype != 1) return hipErrorInvalidValue;
   const float scale_log2 = LOG2E / sqrtf((float)a.hd);
   dim3 grid(a.n_work, a.nh);

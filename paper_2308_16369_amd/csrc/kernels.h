@@ -55,12 +55,13 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s);
 // m the running max of the log2-scaled scores, l the sum of 2^(s - m),
 // o the unnormalised weighted sum of values.
 struct PrefillArgs {
-  const void* qkv;      // chunk rows 0..C-1, q columns rotated
+  const void* qkv;      // all rows; chunk c's rows start at its first-row entry; q columns rotated
   int ld_qkv;
   const void* kv_layer;
   KVStrides st;
-  int slot, offset, C, nh, hd;
-  const int* work;      // [n_work] (q_block << 12) | key_split
+  const int* chunks;    // [n_chunks][slot, offset, len, first row]
+  int nh, hd;
+  const int* work;      // [n_work][chunk, (q_block << 12) | key_split]
   int n_work, split_keys;
   float* part;          // item i, row j of its q-block -> partial index i * 64 + j
 };

@@ -87,55 +87,108 @@ struct Layout {
   size_t a, qkv, o, hres, m, parts, part, meta, ping0, ping1, total;
 };
 
-Layout make_layout(const sarathi_model_cfg* c, int T, int S) {
+// Workspace regions for batches of up to T rows in up to n_chunks prompt
+// chunks (>= 1) with a KV of S positions per slot.
+Layout make_layout(const sarathi_model_cfg* c, int T, int n_chunks, int S) {
   Layout L{};
   const size_t es = esize(c);
   const size_t H = c->hidden, F = c->ffn, QD = (size_t)c->n_heads * c->head_dim;
   size_t off = 0;
   auto take = [&](size_t bytes) { const size_t at = off; off = align256(off + bytes); return at; };
+  if (n_chunks < 1) n_chunks = 1;
   L.a = take(T * H * es);
   L.qkv = take(T * 3 * QD * es);
   L.o = take(T * QD * es);
   L.hres = take(T * H * 4);
   L.m = take(T * F * es);
   L.parts = take((size_t)MAX_SPLIT * T * H * 4);
-  const size_t max_pre = (size_t)((T + QBLOCK - 1) / QBLOCK) * ((S + PRE_SPLIT - 1) / PRE_SPLIT);
+  // query blocks of 64 rows: each chunk starts a new block
+  const size_t max_pre = ((size_t)(T + QBLOCK - 1) / QBLOCK + n_chunks - 1) * ((S + PRE_SPLIT - 1) / PRE_SPLIT);
   const size_t max_dec = (size_t)T * ((S + SPLIT_KEYS - 1) / SPLIT_KEYS);
   L.part = take((max_pre * QBLOCK + max_dec) * c->n_heads * (c->head_dim + 2) * 4);
-  L.meta = take(((size_t)T * 5 + max_pre + max_dec) * 4);
+  L.meta = take(((size_t)T * 5 + (size_t)n_chunks * 4 + max_pre * 2 + max_dec) * 4);
   L.ping0 = take(T * H * es);
   L.ping1 = take(T * H * es);
   L.total = off;
   return L;
 }
 
-// Host-side description of the batch and its device metadata.
-struct Plan {
-  int C, B, T, row_base, n_pre, n_dec;
-  std::vector<int> meta;   // row_slot[T] row_pos[T] comb[3T] pre_work[n_pre] dec_work[n_dec]
-  size_t o_slot, o_pos, o_comb, o_pre, o_dec;   // int offsets into meta
+// A batch of any number of prompt chunks plus decodes (the hybrid batch of
+// the paper has at most one chunk).
+struct ChunkDesc {
+  int slot, offset, len;
+};
+struct BatchDesc {
+  std::vector<ChunkDesc> chunks;
+  int B = 0;
+  const int* dslots = nullptr;
+  const int* dctx = nullptr;
+  int rows() const {
+    int r = B;
+    for (const ChunkDesc& c : chunks) r += c.len;
+    return r;
+  }
 };
 
-int check_batch(const sarathi_model_cfg* cfg, const sarathi_kv* kv, const sarathi_hybrid_batch* b) {
+int from_hybrid(const sarathi_hybrid_batch* b, BatchDesc* out) {
   if (!b) return fail(SARATHI_EINVAL, "batch is NULL");
-  const int C = b->chunk_len, B = b->n_decodes, S = kv->max_seq_len;
-  if (C < 0) return fail(SARATHI_ERANGE, "chunk_len %d < 0", C);
-  if (B < 0) return fail(SARATHI_EINVAL, "n_decodes %d < 0", B);
-  if (C + B == 0) return fail(SARATHI_EINVAL, "empty batch (chunk_len + n_decodes == 0)");
-  if (C + B > (1 << 19)) return fail(SARATHI_EINVAL, "batch of %d rows too large", C + B);
+  if (b->chunk_len < 0) return fail(SARATHI_ERANGE, "chunk_len %d < 0", b->chunk_len);
+  if (b->n_decodes < 0) return fail(SARATHI_EINVAL, "n_decodes %d < 0", b->n_decodes);
+  out->chunks.clear();
+  if (b->chunk_len > 0) out->chunks.push_back({b->prefill_slot, b->chunk_offset, b->chunk_len});
+  out->B = b->n_decodes;
+  out->dslots = b->decode_slots;
+  out->dctx = b->decode_ctx_lens;
+  return SARATHI_OK;
+}
+
+int from_mixed(const sarathi_mixed_batch* b, BatchDesc* out) {
+  if (!b) return fail(SARATHI_EINVAL, "batch is NULL");
+  if (b->n_chunks < 0 || b->n_chunks > (1 << 16)) return fail(SARATHI_EINVAL, "n_chunks %d out of range", b->n_chunks);
+  if (b->n_decodes < 0) return fail(SARATHI_EINVAL, "n_decodes %d < 0", b->n_decodes);
+  if (b->n_chunks > 0 && (!b->chunk_slots || !b->chunk_offsets || !b->chunk_lens))
+    return fail(SARATHI_EINVAL, "chunk arrays are NULL");
+  out->chunks.clear();
+  for (int i = 0; i < b->n_chunks; ++i) {
+    if (b->chunk_lens[i] < 1) return fail(SARATHI_ERANGE, "chunk_lens[%d] = %d < 1", i, b->chunk_lens[i]);
+    out->chunks.push_back({b->chunk_slots[i], b->chunk_offsets[i], b->chunk_lens[i]});
+  }
+  out->B = b->n_decodes;
+  out->dslots = b->decode_slots;
+  out->dctx = b->decode_ctx_lens;
+  return SARATHI_OK;
+}
+
+// Host-side description of the batch and its device metadata.
+struct Plan {
+  int C, B, T, row_base, n_pre, n_dec, n_chunks;
+  // row_slot[T] row_pos[T] comb[3T] chunk table [n_chunks][slot, offset, len, first row]
+  // pre_work[n_pre][chunk, (q_block << 12) | key_split] dec_work[n_dec]
+  std::vector<int> meta;
+  size_t o_slot, o_pos, o_comb, o_chunks, o_pre, o_dec;   // int offsets into meta
+};
+
+int check_batch(const sarathi_model_cfg* cfg, const sarathi_kv* kv, const BatchDesc& b) {
+  const int B = b.B, S = kv->max_seq_len;
+  long rows = B;
+  for (const ChunkDesc& c : b.chunks) rows += c.len;
+  if (rows == 0) return fail(SARATHI_EINVAL, "empty batch (no chunk rows and no decodes)");
+  if (rows > (1 << 19)) return fail(SARATHI_EINVAL, "batch of %ld rows too large", rows);
   std::vector<char> used(kv->n_slots, 0);
-  if (C > 0) {
-    if (b->prefill_slot < 0 || b->prefill_slot >= kv->n_slots)
-      return fail(SARATHI_EINVAL, "prefill_slot %d outside [0, %d)", b->prefill_slot, kv->n_slots);
-    if (b->chunk_offset < 0) return fail(SARATHI_ERANGE, "chunk_offset %d < 0", b->chunk_offset);
-    if ((long)b->chunk_offset + C > S)
-      return fail(SARATHI_ERANGE, "chunk_offset %d + chunk_len %d > max_seq_len %d", b->chunk_offset, C, S);
-    used[b->prefill_slot] = 1;
+  for (size_t i = 0; i < b.chunks.size(); ++i) {
+    const ChunkDesc& c = b.chunks[i];
+    if (c.slot < 0 || c.slot >= kv->n_slots)
+      return fail(SARATHI_EINVAL, "chunk %zu: slot %d outside [0, %d)", i, c.slot, kv->n_slots);
+    if (used[c.slot]) return fail(SARATHI_EINVAL, "slot %d appears twice in the batch", c.slot);
+    used[c.slot] = 1;
+    if (c.offset < 0) return fail(SARATHI_ERANGE, "chunk %zu: offset %d < 0", i, c.offset);
+    if ((long)c.offset + c.len > S)
+      return fail(SARATHI_ERANGE, "chunk %zu: offset %d + length %d > max_seq_len %d", i, c.offset, c.len, S);
   }
   if (B > 0) {
-    if (!b->decode_slots || !b->decode_ctx_lens) return fail(SARATHI_EINVAL, "decode arrays are NULL");
+    if (!b.dslots || !b.dctx) return fail(SARATHI_EINVAL, "decode arrays are NULL");
     for (int i = 0; i < B; ++i) {
-      const int s = b->decode_slots[i], ctx = b->decode_ctx_lens[i];
+      const int s = b.dslots[i], ctx = b.dctx[i];
       if (s < 0 || s >= kv->n_slots) return fail(SARATHI_EINVAL, "decode_slots[%d] = %d outside [0, %d)", i, s, kv->n_slots);
       if (used[s]) return fail(SARATHI_EINVAL, "slot %d appears twice in the batch", s);
       used[s] = 1;
@@ -147,33 +200,44 @@ int check_batch(const sarathi_model_cfg* cfg, const sarathi_kv* kv, const sarath
   return SARATHI_OK;
 }
 
-Plan make_plan(const sarathi_model_cfg* cfg, const sarathi_hybrid_batch* b) {
+Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
   Plan p;
-  p.C = b->chunk_len;
-  p.B = b->n_decodes;
+  p.B = b.B;
+  p.C = b.rows() - b.B;
   p.T = p.C + p.B;
-  // bf16: the chunk goes to the MFMA chunk-attention kernel (work item =
-  // 64-row query block x key split), the decodes to row attention (work item
-  // = row x key split).  fp32: every row goes to row attention (a chunk row
-  // at position p is attention over keys 0..p, like a decode with ctx = p).
+  p.n_chunks = (int)b.chunks.size();
+  // bf16: chunk rows go to the MFMA chunk-attention kernel (work item = one
+  // chunk's 64-row query block x key split), decodes to row attention (work
+  // item = row x key split).  fp32: every row goes to row attention (a chunk
+  // row at position p is attention over keys 0..p, like a decode with ctx = p).
   p.row_base = (cfg->dtype == SARATHI_BF16) ? p.C : 0;
-  std::vector<int> slot(p.T), pos(p.T), comb(3 * p.T), pre, dec;
-  for (int r = 0; r < p.C; ++r) { slot[r] = b->prefill_slot; pos[r] = b->chunk_offset + r; }
-  for (int i = 0; i < p.B; ++i) { slot[p.C + i] = b->decode_slots[i]; pos[p.C + i] = b->decode_ctx_lens[i]; }
+  std::vector<int> slot(p.T), pos(p.T), comb(3 * p.T), tab, pre, dec;
+  int r0 = 0;
+  for (const ChunkDesc& c : b.chunks) {
+    tab.insert(tab.end(), {c.slot, c.offset, c.len, r0});
+    for (int r = 0; r < c.len; ++r) { slot[r0 + r] = c.slot; pos[r0 + r] = c.offset + r; }
+    r0 += c.len;
+  }
+  for (int i = 0; i < p.B; ++i) { slot[p.C + i] = b.dslots[i]; pos[p.C + i] = b.dctx[i]; }
   if (p.row_base > 0) {
-    for (int qb = 0; qb * QBLOCK < p.C; ++qb) {
-      const int n_keys = b->chunk_offset + std::min((qb + 1) * QBLOCK, p.C);
-      const int ns = (n_keys + PRE_SPLIT - 1) / PRE_SPLIT;
-      const int first = (int)pre.size();
-      for (int s = 0; s < ns; ++s) pre.push_back((qb << 12) | s);
-      for (int r = qb * QBLOCK; r < std::min((qb + 1) * QBLOCK, p.C); ++r) {
-        comb[3 * r] = first * QBLOCK + (r - qb * QBLOCK);
-        comb[3 * r + 1] = ns;
-        comb[3 * r + 2] = QBLOCK;
+    r0 = 0;
+    for (int ci = 0; ci < p.n_chunks; ++ci) {
+      const ChunkDesc& c = b.chunks[ci];
+      for (int qb = 0; qb * QBLOCK < c.len; ++qb) {
+        const int n_keys = c.offset + std::min((qb + 1) * QBLOCK, c.len);
+        const int ns = (n_keys + PRE_SPLIT - 1) / PRE_SPLIT;
+        const int first = (int)pre.size() / 2;
+        for (int s = 0; s < ns; ++s) pre.insert(pre.end(), {ci, (qb << 12) | s});
+        for (int r = qb * QBLOCK; r < std::min((qb + 1) * QBLOCK, c.len); ++r) {
+          comb[3 * (r0 + r)] = first * QBLOCK + (r - qb * QBLOCK);
+          comb[3 * (r0 + r) + 1] = ns;
+          comb[3 * (r0 + r) + 2] = QBLOCK;
+        }
       }
+      r0 += c.len;
     }
   }
-  const int pre_rows = (int)pre.size() * QBLOCK;
+  const int pre_rows = (int)pre.size() / 2 * QBLOCK;
   for (int r = p.row_base; r < p.T; ++r) {
     const int ns = (pos[r] + 1 + SPLIT_KEYS - 1) / SPLIT_KEYS;
     comb[3 * r] = pre_rows + (int)dec.size();
@@ -181,12 +245,13 @@ Plan make_plan(const sarathi_model_cfg* cfg, const sarathi_hybrid_batch* b) {
     comb[3 * r + 2] = 1;
     for (int s = 0; s < ns; ++s) dec.push_back(((r - p.row_base) << 12) | s);
   }
-  p.n_pre = (int)pre.size();
+  p.n_pre = (int)pre.size() / 2;
   p.n_dec = (int)dec.size();
-  p.meta.reserve(5 * p.T + pre.size() + dec.size());
+  p.meta.reserve(5 * p.T + tab.size() + pre.size() + dec.size());
   p.o_slot = 0; p.meta.insert(p.meta.end(), slot.begin(), slot.end());
   p.o_pos = p.meta.size(); p.meta.insert(p.meta.end(), pos.begin(), pos.end());
   p.o_comb = p.meta.size(); p.meta.insert(p.meta.end(), comb.begin(), comb.end());
+  p.o_chunks = p.meta.size(); p.meta.insert(p.meta.end(), tab.begin(), tab.end());
   p.o_pre = p.meta.size(); p.meta.insert(p.meta.end(), pre.begin(), pre.end());
   p.o_dec = p.meta.size(); p.meta.insert(p.meta.end(), dec.begin(), dec.end());
   return p;
@@ -297,7 +362,7 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
   if (P.n_pre > 0) {
     PrefillArgs pa{};
     pa.qkv = ws + c.L.qkv; pa.ld_qkv = 3 * QD; pa.kv_layer = kv_layer; pa.st = c.kv->st;
-    pa.slot = c.plan->meta[P.o_slot]; pa.offset = c.plan->meta[P.o_pos]; pa.C = P.C; pa.nh = nh; pa.hd = hd;
+    pa.chunks = meta + P.o_chunks; pa.nh = nh; pa.hd = hd;
     pa.work = meta + P.o_pre; pa.n_work = P.n_pre; pa.split_keys = PRE_SPLIT; pa.part = part;
     e = launch_attn_prefill(dt, pa, c.s);
     if (e != hipSuccess) return hip_fail(e, "chunk attention");
@@ -353,7 +418,7 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
 }
 
 int prepare(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, int n_w, sarathi_kv* kv,
-            const sarathi_hybrid_batch* batch, const void* x_in, void* x_out, void* ws, size_t ws_bytes,
+            const BatchDesc& batch, const void* x_in, void* x_out, void* ws, size_t ws_bytes,
             Plan* plan, Layout* L) {
   int rc = check_cfg(cfg);
   if (rc) return rc;
@@ -370,8 +435,8 @@ int prepare(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, int n_
   if (x_in == x_out) return fail(SARATHI_EINVAL, "x_in and x_out alias");
   if (!aligned16(x_in) || !aligned16(x_out) || !aligned16(ws))
     return fail(SARATHI_EINVAL, "x_in, x_out and ws must be 16-byte aligned");
-  const int T = batch->chunk_len + batch->n_decodes;
-  *L = make_layout(cfg, T, kv->max_seq_len);
+  const int T = batch.rows();
+  *L = make_layout(cfg, T, (int)batch.chunks.size(), kv->max_seq_len);
   if (ws_bytes < L->total)
     return fail(SARATHI_ENOSPC, "workspace of %zu bytes < %zu needed", ws_bytes, L->total);
   const char* wb = static_cast<const char*>(ws);
@@ -438,28 +503,31 @@ int sarathi_kv_get_strides(const sarathi_kv* kv, sarathi_kv_strides* out) {
 size_t sarathi_workspace_bytes(const sarathi_model_cfg* cfg, int max_tokens, int max_decodes, int max_seq_len) {
   if (check_cfg(cfg) != SARATHI_OK || max_tokens < 1 || max_decodes < 0 || max_seq_len < 1) return 0;
   (void)max_decodes;
-  return make_layout(cfg, max_tokens, max_seq_len).total;
+  return make_layout(cfg, max_tokens, 1, max_seq_len).total;
 }
 
-int sarathi_workspace_layout(const sarathi_model_cfg* cfg, int n_tokens, int n_decodes, int max_seq_len,
-                             sarathi_ws_layout* out) {
+size_t sarathi_mixed_workspace_bytes(const sarathi_model_cfg* cfg, int max_tokens, int max_chunks, int max_seq_len) {
+  if (check_cfg(cfg) != SARATHI_OK || max_tokens < 1 || max_chunks < 0 || max_seq_len < 1) return 0;
+  return make_layout(cfg, max_tokens, max_chunks, max_seq_len).total;
+}
+
+namespace {
+int layout_out(const sarathi_model_cfg* cfg, int n_tokens, int n_chunks, int max_seq_len, sarathi_ws_layout* out) {
   int rc = check_cfg(cfg);
   if (rc) return rc;
   if (!out) return fail(SARATHI_EINVAL, "out is NULL");
-  if (n_tokens < 1 || n_decodes < 0 || n_decodes > n_tokens || max_seq_len < 1)
-    return fail(SARATHI_EINVAL, "bad sizes");
-  const Layout L = make_layout(cfg, n_tokens, max_seq_len);
+  if (n_tokens < 1 || n_chunks < 0 || max_seq_len < 1) return fail(SARATHI_EINVAL, "bad sizes");
+  const Layout L = make_layout(cfg, n_tokens, n_chunks, max_seq_len);
   out->a = L.a; out->qkv = L.qkv; out->o = L.o; out->hres = L.hres; out->m = L.m;
   out->ping[0] = L.ping0; out->ping[1] = L.ping1; out->total = L.total;
   return SARATHI_OK;
 }
 
-int sarathi_hybrid_layer_forward(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, sarathi_kv* kv,
-                                 int layer, const sarathi_hybrid_batch* batch, const void* x_in, void* x_out,
-                                 void* ws, size_t ws_bytes, void* hip_stream) {
+int run_layer(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, sarathi_kv* kv, int layer,
+              const BatchDesc& b, const void* x_in, void* x_out, void* ws, size_t ws_bytes, void* hip_stream) {
   Plan plan;
   Layout L;
-  int rc = prepare(cfg, w, 1, kv, batch, x_in, x_out, ws, ws_bytes, &plan, &L);
+  int rc = prepare(cfg, w, 1, kv, b, x_in, x_out, ws, ws_bytes, &plan, &L);
   if (rc) return rc;
   if (layer < 0 || layer >= cfg->n_layers) return fail(SARATHI_EINVAL, "layer %d outside [0, %d)", layer, cfg->n_layers);
   Ctx c{cfg, kv, &plan, L, static_cast<char*>(ws), static_cast<hipStream_t>(hip_stream)};
@@ -468,13 +536,11 @@ int sarathi_hybrid_layer_forward(const sarathi_model_cfg* cfg, const sarathi_lay
   return layer_body(c, w, layer, x_in, x_out);
 }
 
-int sarathi_model_step(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, sarathi_kv* kv,
-                       const sarathi_hybrid_batch* batch, const void* x_in, void* x_out, void* ws,
-                       size_t ws_bytes, void* hip_stream) {
-  if (!cfg) return fail(SARATHI_EINVAL, "cfg is NULL");
+int run_model(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, sarathi_kv* kv, const BatchDesc& b,
+              const void* x_in, void* x_out, void* ws, size_t ws_bytes, void* hip_stream) {
   Plan plan;
   Layout L;
-  int rc = prepare(cfg, w, cfg->n_layers > 0 ? cfg->n_layers : 0, kv, batch, x_in, x_out, ws, ws_bytes, &plan, &L);
+  int rc = prepare(cfg, w, cfg->n_layers > 0 ? cfg->n_layers : 0, kv, b, x_in, x_out, ws, ws_bytes, &plan, &L);
   if (rc) return rc;
   Ctx c{cfg, kv, &plan, L, static_cast<char*>(ws), static_cast<hipStream_t>(hip_stream)};
   rc = upload_meta(c);
@@ -488,6 +554,56 @@ int sarathi_model_step(const sarathi_model_cfg* cfg, const sarathi_layer_weights
     if (rc) return rc;
   }
   return SARATHI_OK;
+}
+}  // namespace
+
+int sarathi_workspace_layout(const sarathi_model_cfg* cfg, int n_tokens, int n_decodes, int max_seq_len,
+                             sarathi_ws_layout* out) {
+  if (n_decodes < 0 || n_decodes > n_tokens) return fail(SARATHI_EINVAL, "bad sizes");
+  return layout_out(cfg, n_tokens, 1, max_seq_len, out);
+}
+
+int sarathi_mixed_workspace_layout(const sarathi_model_cfg* cfg, int n_tokens, int n_chunks, int max_seq_len,
+                                   sarathi_ws_layout* out) {
+  return layout_out(cfg, n_tokens, n_chunks, max_seq_len, out);
+}
+
+int sarathi_hybrid_layer_forward(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, sarathi_kv* kv,
+                                 int layer, const sarathi_hybrid_batch* batch, const void* x_in, void* x_out,
+                                 void* ws, size_t ws_bytes, void* hip_stream) {
+  BatchDesc b;
+  int rc = from_hybrid(batch, &b);
+  if (rc) return rc;
+  return run_layer(cfg, w, kv, layer, b, x_in, x_out, ws, ws_bytes, hip_stream);
+}
+
+int sarathi_model_step(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, sarathi_kv* kv,
+                       const sarathi_hybrid_batch* batch, const void* x_in, void* x_out, void* ws,
+                       size_t ws_bytes, void* hip_stream) {
+  if (!cfg) return fail(SARATHI_EINVAL, "cfg is NULL");
+  BatchDesc b;
+  int rc = from_hybrid(batch, &b);
+  if (rc) return rc;
+  return run_model(cfg, w, kv, b, x_in, x_out, ws, ws_bytes, hip_stream);
+}
+
+int sarathi_mixed_layer_forward(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, sarathi_kv* kv,
+                                int layer, const sarathi_mixed_batch* batch, const void* x_in, void* x_out,
+                                void* ws, size_t ws_bytes, void* hip_stream) {
+  BatchDesc b;
+  int rc = from_mixed(batch, &b);
+  if (rc) return rc;
+  return run_layer(cfg, w, kv, layer, b, x_in, x_out, ws, ws_bytes, hip_stream);
+}
+
+int sarathi_mixed_model_step(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, sarathi_kv* kv,
+                             const sarathi_mixed_batch* batch, const void* x_in, void* x_out, void* ws,
+                             size_t ws_bytes, void* hip_stream) {
+  if (!cfg) return fail(SARATHI_EINVAL, "cfg is NULL");
+  BatchDesc b;
+  int rc = from_mixed(batch, &b);
+  if (rc) return rc;
+  return run_model(cfg, w, kv, b, x_in, x_out, ws, ws_bytes, hip_stream);
 }
 
 int sarathi_profile_begin(int max_calls) {

@@ -55,6 +55,12 @@ class sarathi_hybrid_batch(ct.Structure):
                 ("decode_ctx_lens", ct.POINTER(ct.c_int))]
 
 
+class sarathi_mixed_batch(ct.Structure):
+    _fields_ = [("n_chunks", ct.c_int), ("chunk_slots", ct.POINTER(ct.c_int)), ("chunk_offsets", ct.POINTER(ct.c_int)),
+                ("chunk_lens", ct.POINTER(ct.c_int)), ("n_decodes", ct.c_int), ("decode_slots", ct.POINTER(ct.c_int)),
+                ("decode_ctx_lens", ct.POINTER(ct.c_int))]
+
+
 class sarathi_kv_strides(ct.Structure):
     _fields_ = [(n, ct.c_size_t) for n in ("layer", "slot", "kv", "head", "pos")]
 
@@ -99,6 +105,15 @@ EXPORTS = {
     "sarathi_model_step": (ct.c_int, [ct.POINTER(sarathi_model_cfg), ct.POINTER(sarathi_layer_weights),
                                       ct.c_void_p, ct.POINTER(sarathi_hybrid_batch), ct.c_void_p, ct.c_void_p,
                                       ct.c_void_p, ct.c_size_t, ct.c_void_p]),
+    "sarathi_mixed_workspace_bytes": (ct.c_size_t, [ct.POINTER(sarathi_model_cfg), ct.c_int, ct.c_int, ct.c_int]),
+    "sarathi_mixed_workspace_layout": (ct.c_int, [ct.POINTER(sarathi_model_cfg), ct.c_int, ct.c_int, ct.c_int,
+                                                  ct.POINTER(sarathi_ws_layout)]),
+    "sarathi_mixed_layer_forward": (ct.c_int, [ct.POINTER(sarathi_model_cfg), ct.POINTER(sarathi_layer_weights),
+                                               ct.c_void_p, ct.c_int, ct.POINTER(sarathi_mixed_batch),
+                                               ct.c_void_p, ct.c_void_p, ct.c_void_p, ct.c_size_t, ct.c_void_p]),
+    "sarathi_mixed_model_step": (ct.c_int, [ct.POINTER(sarathi_model_cfg), ct.POINTER(sarathi_layer_weights),
+                                            ct.c_void_p, ct.POINTER(sarathi_mixed_batch), ct.c_void_p, ct.c_void_p,
+                                            ct.c_void_p, ct.c_size_t, ct.c_void_p]),
     "sarathi_profile_begin": (ct.c_int, [ct.c_int]),
     "sarathi_profile_end": (ct.c_int, [ct.POINTER(ct.c_double), ct.POINTER(ct.c_int)]),
     "sarathi_linear_scratch_bytes": (ct.c_size_t, [ct.c_int, ct.c_int]),
@@ -230,6 +245,44 @@ def sarathi_model_step(cfg, weights: Sequence[sarathi_layer_weights], kv: KV, ba
     return _check(rc) if check else rc
 
 
+def sarathi_mixed_workspace_bytes(cfg, max_tokens, max_chunks, max_seq_len) -> int:
+    return lib().sarathi_mixed_workspace_bytes(ct.byref(cfg), max_tokens, max_chunks, max_seq_len)
+
+
+def sarathi_mixed_workspace_layout(cfg, n_tokens, n_chunks, max_seq_len) -> sarathi_ws_layout:
+    out = sarathi_ws_layout()
+    _check(lib().sarathi_mixed_workspace_layout(ct.byref(cfg), n_tokens, n_chunks, max_seq_len, ct.byref(out)))
+    return out
+
+
+def make_mixed_batch(chunks: Sequence[Sequence[int]], decode_slots: Sequence[int], decode_ctx: Sequence[int]):
+    """Build a sarathi_mixed_batch from chunks [(slot, offset, len)] and
+    decodes; returns (struct, keepalive arrays)."""
+    k, n = len(chunks), len(decode_slots)
+    arr = lambda vals, m: (ct.c_int * max(m, 1))(*[int(v) for v in vals])
+    cs, co, cl = arr([c[0] for c in chunks], k), arr([c[1] for c in chunks], k), arr([c[2] for c in chunks], k)
+    ds, dc = arr(decode_slots, n), arr(decode_ctx, n)
+    P = lambda a: ct.cast(a, ct.POINTER(ct.c_int))
+    b = sarathi_mixed_batch(k, P(cs), P(co), P(cl), n, P(ds), P(dc))
+    return b, (cs, co, cl, ds, dc)
+
+
+def sarathi_mixed_layer_forward(cfg, weights: sarathi_layer_weights, kv: KV, layer: int, batch, x_in: int,
+                                x_out: int, ws: int, ws_bytes: int, stream: int = 0, check: bool = True) -> int:
+    rc = lib().sarathi_mixed_layer_forward(ct.byref(cfg), ct.byref(weights), kv.handle, layer, ct.byref(batch),
+                                           ct.c_void_p(x_in), ct.c_void_p(x_out), ct.c_void_p(ws), ws_bytes,
+                                           ct.c_void_p(stream))
+    return _check(rc) if check else rc
+
+
+def sarathi_mixed_model_step(cfg, weights: Sequence[sarathi_layer_weights], kv: KV, batch, x_in: int, x_out: int,
+                             ws: int, ws_bytes: int, stream: int = 0, check: bool = True) -> int:
+    arr = (sarathi_layer_weights * len(weights))(*weights)
+    rc = lib().sarathi_mixed_model_step(ct.byref(cfg), arr, kv.handle, ct.byref(batch), ct.c_void_p(x_in),
+                                        ct.c_void_p(x_out), ct.c_void_p(ws), ws_bytes, ct.c_void_p(stream))
+    return _check(rc) if check else rc
+
+
 N_STAGES = 10
 STAGE_NAMES = ["norm_1", "preproj", "rope_kv_append", "chunk_attention", "decode_attention", "attention_combine",
                "postproj", "norm_2",
@@ -283,6 +336,11 @@ class Step:
     @property
     def n_decodes(self) -> int:
         return len(self.decode_ctx)
+
+    def mixed_batch(self):
+        """(sarathi_mixed_batch, keepalive) for any iteration."""
+        return make_mixed_batch(list(zip(self.chunk_slot, self.chunk_offset, self.chunk_len)), self.decode_slot,
+                                self.decode_ctx)
 
     def hybrid_batch(self):
         """(sarathi_hybrid_batch, keepalive) for an iteration of at most one chunk."""

@@ -40,7 +40,7 @@ class ServeModel:
     the device (0.02 * N(0,1); gains 1 + 0.02 * N(0,1))."""
 
     def __init__(self, shape, n_layers: int, n_slots: int, max_seq_len: int, max_tokens: int,
-                 weights: Optional[List[dict]] = None, seed: int = 0):
+                 weights: Optional[List[dict]] = None, seed: int = 0, max_chunks: int = 1):
         import numpy as np
         import torch
 
@@ -74,20 +74,21 @@ class ServeModel:
         self.kv_t = torch.zeros((n_layers, n_slots, 2, nh, max_seq_len, d), dtype=self.tdt, device="cuda")
         self.kv = S.sarathi_kv_alloc(self.cfg, n_slots, max_seq_len, self.kv_t.data_ptr(),
                                      self.kv_t.numel() * self.kv_t.element_size())
-        self.n_slots, self.max_seq_len, self.max_tokens = n_slots, max_seq_len, max_tokens
-        self.ws_bytes = S.sarathi_workspace_bytes(self.cfg, max_tokens, max_tokens, max_seq_len)
+        self.n_slots, self.max_seq_len, self.max_tokens, self.max_chunks = n_slots, max_seq_len, max_tokens, max_chunks
+        self.ws_bytes = S.sarathi_mixed_workspace_bytes(self.cfg, max_tokens, max_chunks, max_seq_len)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device="cuda")
         self.x = torch.empty((max_tokens, H), dtype=self.tdt, device="cuda").normal_(0.0, 1.0, generator=g)
         self.y = torch.empty_like(self.x)
         self.stream = torch.cuda.current_stream()
 
     def step(self, bb, x, y):
+        """One model iteration over a sarathi_mixed_batch (any number of chunks)."""
         lib = S.lib()
         import ctypes as ct
-        rc = lib.sarathi_model_step(ct.byref(self.cfg), self.wabi, self.kv.handle, ct.byref(bb),
-                                    ct.c_void_p(x.data_ptr()), ct.c_void_p(y.data_ptr()),
-                                    ct.c_void_p(self.ws.data_ptr()), self.ws_bytes,
-                                    ct.c_void_p(self.stream.cuda_stream))
+        rc = lib.sarathi_mixed_model_step(ct.byref(self.cfg), self.wabi, self.kv.handle, ct.byref(bb),
+                                          ct.c_void_p(x.data_ptr()), ct.c_void_p(y.data_ptr()),
+                                          ct.c_void_p(self.ws.data_ptr()), self.ws_bytes,
+                                          ct.c_void_p(self.stream.cuda_stream))
         S._check(rc)
 
 
@@ -113,9 +114,10 @@ def run_schedule(m: ServeModel, policy: int, requests: Sequence[Tuple[int, int]]
         st = sched.next()
         if st.n_tokens == 0:
             break
-        if st.n_tokens > m.max_tokens:
-            raise ValueError(f"an iteration of {st.n_tokens} rows exceeds the workspace ({m.max_tokens})")
-        bb, keep = st.hybrid_batch()
+        if st.n_tokens > m.max_tokens or st.n_chunks > m.max_chunks:
+            raise ValueError(f"an iteration of {st.n_tokens} rows in {st.n_chunks} chunks exceeds the workspace "
+                             f"({m.max_tokens} rows, {m.max_chunks} chunks)")
+        bb, keep = st.mixed_batch()
         x, y = m.x[:st.n_tokens], m.y[:st.n_tokens]
         if inputs is not None:
             rows = _rows(st)
@@ -158,18 +160,27 @@ def pd_split(seq_len: int, ratio: float) -> Tuple[int, int]:
 
 
 def sweep(m: ServeModel, seq_len: int, ratios: Sequence[float], chunks: Sequence[int], max_batch: int,
-          n_requests: int, log=lambda s: None) -> List[dict]:
+          n_requests: int, log=lambda s: None, mixed: bool = False) -> List[dict]:
+    """Decode-maximal (each chunk size) against the prefill/decode baseline
+    for each P:D ratio; with ``mixed``, also Orca-style mixed batching (whole
+    prompts of up to m.max_chunks requests plus every decode, within
+    m.max_tokens rows)."""
     out = []
     for ratio in ratios:
         P, D = pd_split(seq_len, ratio)
         reqs = [(P, D)] * n_requests
         base = run_schedule(m, S.POLICY_PREFILL_DECODE, reqs, max_batch, 0)
+        mix = None
+        if mixed:
+            mix = run_schedule(m, S.POLICY_MIXED, reqs, max_batch, 0, max_chunks=m.max_chunks,
+                               max_tokens=m.max_tokens - max_batch)
         for C in chunks:
             dm = run_schedule(m, S.POLICY_DECODE_MAXIMAL, reqs, max_batch, C)
             out.append({"seq_len": seq_len, "P": P, "D": D, "pd": round(P / D, 2), "B": max_batch, "C": C,
                         "n_requests": n_requests, "peak_pd": round(C / max(1, max_batch - 1), 2),
-                        "decode_maximal": dm, "baseline": base,
-                        "speedup": round(dm["tokens_per_s"] / base["tokens_per_s"], 3)})
+                        "decode_maximal": dm, "baseline": base, "mixed": mix,
+                        "speedup": round(dm["tokens_per_s"] / base["tokens_per_s"], 3),
+                        "mixed_speedup": round(mix["tokens_per_s"] / base["tokens_per_s"], 3) if mix else None})
             log(f"seq {seq_len} P:D {P}:{D} C {C}: {dm['tokens_per_s']:.0f} vs {base['tokens_per_s']:.0f} tok/s "
                 f"({out[-1]['speedup']}x)")
     return out
@@ -179,12 +190,13 @@ def to_markdown(res: dict) -> str:
     L = [f"# End-to-end throughput vs P:D: {res['workload']}", "", f"Command: `{res['command']}`", "",
          res["note"], "",
          "| seq | P | D | P:D | B | C | C/(B-1) | decode-maximal tok/s | baseline tok/s | speedup | "
-         "hybrid / prefill-only / decode-only iterations |",
-         "|---|---|---|---|---|---|---|---|---|---|---|"]
+         "mixed tok/s (speedup) | hybrid / prefill-only / decode-only iterations |",
+         "|---|---|---|---|---|---|---|---|---|---|---|---|"]
     for e in res["sweep"]:
-        dm, b = e["decode_maximal"], e["baseline"]
+        dm, b, mx = e["decode_maximal"], e["baseline"], e.get("mixed")
+        mixed = f"{mx['tokens_per_s']:.0f} ({e['mixed_speedup']:.3f})" if mx else "-"
         L.append(f"| {e['seq_len']} | {e['P']} | {e['D']} | {e['pd']} | {e['B']} | {e['C']} | {e['peak_pd']} | "
-                 f"{dm['tokens_per_s']:.0f} | {b['tokens_per_s']:.0f} | {e['speedup']:.3f} | "
+                 f"{dm['tokens_per_s']:.0f} | {b['tokens_per_s']:.0f} | {e['speedup']:.3f} | {mixed} | "
                  f"{dm['hybrid_iterations']} / {dm['prefill_only_iterations']} / {dm['decode_only_iterations']} |")
     return "\n".join(L) + "\n"
 
@@ -197,6 +209,8 @@ def main(argv: Optional[Sequence[str]] = None) -> int:
     ap.add_argument("--chunks", type=int, nargs="+", default=[128, 256, 512])
     ap.add_argument("--ratios", type=float, nargs="+", default=[1, 2, 4, 8, 14, 28, 50, 100])
     ap.add_argument("--requests", type=int, default=0, help="requests per run (default 2 x batch)")
+    ap.add_argument("--mixed", action="store_true", help="also run Orca-style mixed batching")
+    ap.add_argument("--mixed-chunks", type=int, default=4, help="prompts per mixed iteration")
     ap.add_argument("--json", default=None)
     ap.add_argument("--md", default=None)
     args = ap.parse_args(argv)
@@ -210,9 +224,13 @@ def main(argv: Optional[Sequence[str]] = None) -> int:
     n_req = args.requests or 2 * args.batch
     max_seq = max(args.seq)
     max_tokens = max(max(args.seq), max(args.chunks) + args.batch)
+    max_chunks = 1
+    if args.mixed:
+        max_chunks = args.mixed_chunks
+        max_tokens = max(max_tokens, args.mixed_chunks * max(args.seq) + args.batch)
     t0 = time.time()
     log = lambda s: print(f"# {s} ({time.time() - t0:.1f}s)", file=sys.stderr, flush=True)
-    m = ServeModel(shape, args.layers, args.batch, max_seq, max_tokens)
+    m = ServeModel(shape, args.layers, args.batch, max_seq, max_tokens, max_chunks=max_chunks)
     log(f"{args.layers}-layer model on the device")
     run_schedule(m, S.POLICY_DECODE_MAXIMAL, [(64, 4)] * 2, 2, 32)     # warm-up
     res = {"workload": f"llama13b-{args.layers}layers-bf16", "command":
@@ -222,7 +240,7 @@ def main(argv: Optional[Sequence[str]] = None) -> int:
                    f"hidden states stand in for tokens.",
            "sweep": []}
     for seq in args.seq:
-        res["sweep"] += sweep(m, seq, args.ratios, args.chunks, args.batch, n_req, log)
+        res["sweep"] += sweep(m, seq, args.ratios, args.chunks, args.batch, n_req, log, mixed=args.mixed)
     if args.json:
         with open(args.json, "w") as f:
             json.dump(res, f, indent=1)

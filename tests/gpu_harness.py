@@ -86,7 +86,7 @@ WKEYS = ("norm1_g", "norm1_b", "w_qkv", "w_o", "norm2_g", "norm2_b", "w_up", "w_
 class DeviceModel:
     """Weights, KV and workspace of an instance on the GPU."""
 
-    def __init__(self, inst: wl.HostInstance, max_tokens: Optional[int] = None):
+    def __init__(self, inst: wl.HostInstance, max_tokens: Optional[int] = None, max_chunks: int = 1):
         self.inst = inst
         shp = inst.shape
         self.dtype = shp.dtype
@@ -102,7 +102,7 @@ class DeviceModel:
         self.kv = S.sarathi_kv_alloc(self.cfg, self.n_slots, self.S, self.kv_dev.data_ptr(),
                                      self.kv_dev.numel() * self.kv_dev.element_size())
         T = max_tokens or inst.batch.n_tokens
-        self.ws_bytes = S.sarathi_workspace_bytes(self.cfg, T, T, self.S)
+        self.ws_bytes = S.sarathi_mixed_workspace_bytes(self.cfg, T, max_chunks, self.S)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device="cuda")
 
     def batch_abi(self, b: wl.Batch):
@@ -114,6 +114,20 @@ class DeviceModel:
         S.sarathi_hybrid_layer_forward(self.cfg, self.w_abi[layer], self.kv, layer, bb, x.data_ptr(),
                                        out.data_ptr(), self.ws.data_ptr(), self.ws_bytes,
                                        torch.cuda.current_stream().cuda_stream)
+        return out
+
+    def mixed_layer(self, layer: int, b: wl.MixedBatch, x: torch.Tensor) -> torch.Tensor:
+        out = torch.empty_like(x)
+        mb, keep = S.make_mixed_batch(b.chunks, list(b.decode_slots), list(b.decode_ctx))
+        S.sarathi_mixed_layer_forward(self.cfg, self.w_abi[layer], self.kv, layer, mb, x.data_ptr(), out.data_ptr(),
+                                      self.ws.data_ptr(), self.ws_bytes, torch.cuda.current_stream().cuda_stream)
+        return out
+
+    def mixed_step(self, b: wl.MixedBatch, x: torch.Tensor) -> torch.Tensor:
+        out = torch.empty_like(x)
+        mb, keep = S.make_mixed_batch(b.chunks, list(b.decode_slots), list(b.decode_ctx))
+        S.sarathi_mixed_model_step(self.cfg, self.w_abi, self.kv, mb, x.data_ptr(), out.data_ptr(),
+                                   self.ws.data_ptr(), self.ws_bytes, torch.cuda.current_stream().cuda_stream)
         return out
 
     def step(self, b: wl.Batch, x: torch.Tensor) -> torch.Tensor:
@@ -143,7 +157,11 @@ class DeviceModel:
         }
 
 
-def oracle_batch(b: wl.Batch) -> oracle.OracleBatch:
+def oracle_batch(b):
+    if isinstance(b, wl.MixedBatch):
+        return oracle.OracleMixedBatch(chunks=[tuple(int(v) for v in c) for c in b.chunks],
+                                       decode_slots=[int(s) for s in b.decode_slots],
+                                       decode_ctx=[int(c) for c in b.decode_ctx])
     return oracle.OracleBatch(prefill_slot=b.prefill_slot, chunk_offset=b.chunk_offset, chunk_len=b.chunk_len,
                               decode_slots=[int(s) for s in b.decode_slots],
                               decode_ctx=[int(c) for c in b.decode_ctx])

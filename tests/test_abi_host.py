@@ -128,6 +128,53 @@ def test_forward_rejects_bad_batches(lib, batch, code):
     assert rc == code, S.sarathi_last_error()
 
 
+@pytest.mark.parametrize("chunks,decodes,code", [
+    ([], ([], []), S.EINVAL),                                  # empty batch
+    ([(1, 0, 4), (1, 8, 4)], ([], []), S.EINVAL),             # one slot in two chunks
+    ([(1, 0, 4), (2, 0, 0)], ([], []), S.ERANGE),             # empty chunk
+    ([(1, 0, 4), (9, 0, 4)], ([], []), S.EINVAL),             # slot out of range
+    ([(1, 0, 4), (2, 250, 7)], ([], []), S.ERANGE),           # offset + len > max_seq_len
+    ([(1, 0, 4), (2, -3, 7)], ([], []), S.ERANGE),            # negative offset
+    ([(1, 0, 4), (2, 0, 7)], ([2], [5]), S.EINVAL),           # decode slot == a chunk's slot
+    ([(1, 0, 4), (2, 0, 7)], ([3], [256]), S.ERANGE),         # ctx + 1 > max_seq_len
+])
+def test_mixed_forward_rejects_bad_batches(lib, chunks, decodes, code):
+    s = Setup(lib)
+    b, keep = S.make_mixed_batch(chunks, *decodes)
+    ws = S.sarathi_mixed_workspace_bytes(s.cfg, 128, 4, 256)
+    rc = S.sarathi_mixed_layer_forward(s.cfg, s.w, s.kv, 0, b, 0x200000, 0x300000, 0x40000000, ws, check=False)
+    assert rc == code, S.sarathi_last_error()
+    rc = S.sarathi_mixed_model_step(s.cfg, [s.w, s.w], s.kv, b, 0x200000, 0x300000, 0x40000000, ws, check=False)
+    assert rc == code, S.sarathi_last_error()
+
+
+def test_mixed_batch_bad_header_fields(lib):
+    s = Setup(lib)
+    b, keep = S.make_mixed_batch([(1, 0, 4)], [], [])
+    b.n_chunks = -1
+    ws = S.sarathi_mixed_workspace_bytes(s.cfg, 128, 4, 256)
+    assert S.sarathi_mixed_layer_forward(s.cfg, s.w, s.kv, 0, b, 0x200000, 0x300000, 0x40000000, ws,
+                                         check=False) == S.EINVAL
+    b.n_chunks = 2
+    b.chunk_lens = ct.cast(None, ct.POINTER(ct.c_int))
+    assert S.sarathi_mixed_layer_forward(s.cfg, s.w, s.kv, 0, b, 0x200000, 0x300000, 0x40000000, ws,
+                                         check=False) == S.EINVAL
+
+
+def test_mixed_workspace_grows_with_chunks_and_matches_hybrid(lib):
+    cfg = tiny_cfg(dtype=S.BF16)
+    one = S.sarathi_mixed_workspace_bytes(cfg, 300, 1, 512)
+    assert one == S.sarathi_workspace_bytes(cfg, 300, 8, 512)
+    assert S.sarathi_mixed_workspace_bytes(cfg, 300, 5, 512) > one
+    L1, L5 = S.sarathi_mixed_workspace_layout(cfg, 300, 1, 512), S.sarathi_mixed_workspace_layout(cfg, 300, 5, 512)
+    assert (L1.a, L1.qkv, L1.o, L1.hres, L1.m) == (L5.a, L5.qkv, L5.o, L5.hres, L5.m)
+    s = Setup(lib)
+    b, keep = S.make_mixed_batch([(1, 0, 40), (2, 0, 40), (3, 0, 40)], [], [])
+    small = S.sarathi_mixed_workspace_bytes(s.cfg, 120, 1, 256)
+    assert S.sarathi_mixed_layer_forward(s.cfg, s.w, s.kv, 0, b, 0x200000, 0x300000, 0x40000000, small,
+                                         check=False) == S.ENOSPC      # sized for one chunk, three given
+
+
 def test_forward_accepts_edge_positions_up_to_validation(lib):
     # offset + C == max_seq_len and ctx + 1 == max_seq_len are legal: only the
     # workspace is too small here, so validation gets all the way to ENOSPC.

@@ -183,6 +183,57 @@ def test_layer_long_chunk_bf16(C, off, decodes):
     run_and_check(wl.make_instance(shape, b, max_seq_len=3072, n_slots=3, seed=41), f"long chunk {C}@{off}")
 
 
+MIXED = {
+    # name: (chunks [(slot, offset, len)], decodes [(slot, ctx)], max_seq_len, n_slots)
+    "three_chunks_and_decodes": ([(2, 100, 37), (0, 0, 64), (5, 190, 65)], [(1, 77), (3, 0), (7, 250)], 256, 9),
+    "chunks_only": ([(4, 0, 1), (6, 255, 1), (8, 128, 100)], [], 256, 9),
+    "many_small_chunks": ([(i, 3 * i, 5 + i) for i in range(6)], [(7, 10), (8, 200)], 256, 9),
+    "long_and_split": ([(0, 300, 200), (1, 0, 129)], [(2, 511), (3, 256)], 512, 4),
+}
+
+
+def run_mixed_and_check(inst, label, layer=0):
+    b = inst.batch
+    log(f"{label}: T={b.n_tokens} chunks={b.chunks} B={b.n_decodes} dtype={inst.shape.dtype}")
+    dm = DeviceModel(inst, max_chunks=max(1, len(b.chunks)))
+    x = to_dev(inst.x, inst.shape.dtype)
+    before = bits_of(dm.kv_dev)
+    y = dm.mixed_layer(layer, b, x)
+    torch.cuda.synchronize()
+    ref = oracle.layer_forward(inst.shape, inst.weights[layer], inst.kv[layer].copy(), oracle_batch(b), inst.x)
+    checks = compare_layer(dm, layer, b, inst.x.astype(np.float64), y, before, inst.kv[layer], ref)
+    assert_checks(checks, label)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("case", list(MIXED))
+def test_mixed_batch_layer(dtype, case):
+    """Several prompt chunks in one layer call (Sec. 5.2's mixed batching):
+    each chunk attends over its own slot, decodes over theirs."""
+    chunks, decs, S_, ns = MIXED[case]
+    shape = _tiny_shape(dtype, hidden=512, n_heads=4, head_dim=128, ffn=1376) if case == "long_and_split" \
+        else _tiny_shape(dtype)
+    b = wl.MixedBatch(chunks=chunks, decode_slots=np.array([d[0] for d in decs], np.int32),
+                      decode_ctx=np.array([d[1] for d in decs], np.int32))
+    run_mixed_and_check(wl.make_instance(shape, b, max_seq_len=S_, n_slots=ns, seed=17), f"mixed {case} {dtype}")
+
+
+def test_mixed_model_step_three_layers_bf16():
+    shape = dataclasses.replace(_tiny_shape("bf16"), n_layers=3)
+    chunks, decs, S_, ns = MIXED["three_chunks_and_decodes"]
+    b = wl.MixedBatch(chunks=chunks, decode_slots=np.array([d[0] for d in decs], np.int32),
+                      decode_ctx=np.array([d[1] for d in decs], np.int32))
+    inst = wl.make_instance(shape, b, max_seq_len=S_, n_slots=ns, seed=23, n_layers=3)
+    dm = DeviceModel(inst, max_chunks=3)
+    y = dm.mixed_step(b, to_dev(inst.x, "bf16"))
+    torch.cuda.synchronize()
+    okv = inst.kv.astype(np.float64)
+    outs = oracle.model_step(shape, inst.weights, okv, oracle_batch(b), inst.x)
+    err = rel_err(from_dev(y), outs[-1].y)
+    log(f"mixed model step bf16: y {err:.3e}")
+    assert err <= TOL["bf16"]
+
+
 # ============================================================================ method invariants on the GPU
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])

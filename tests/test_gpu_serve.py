@@ -34,7 +34,8 @@ def setup(dtype, n_layers, seed):
     X = rng.standard_normal((len(REQS), maxlen, shape.hidden)).astype(np.float32)
     if dtype == "bf16":
         X = wl.round_to_bf16(X)
-    m = serve.ServeModel(shape, n_layers, n_slots=3, max_seq_len=maxlen, max_tokens=128, weights=weights)
+    m = serve.ServeModel(shape, n_layers, n_slots=3, max_seq_len=maxlen, max_tokens=256, weights=weights,
+                         max_chunks=3)
     xin = torch.from_numpy(X).to(m.tdt).cuda()
     return shape, weights, X, m, xin
 
@@ -49,9 +50,9 @@ def oracle_outputs(shape, weights, X):
     return outs
 
 
-def serve_outputs(m, xin, policy, B, C):
+def serve_outputs(m, xin, policy, B, C, **kw):
     out = torch.full_like(xin, float("nan"))
-    res = serve.run_schedule(m, policy, REQS, B, C, inputs=xin, outputs=out)
+    res = serve.run_schedule(m, policy, REQS, B, C, inputs=xin, outputs=out, **kw)
     torch.cuda.synchronize()
     return from_dev(out), res
 
@@ -60,14 +61,15 @@ def serve_outputs(m, xin, policy, B, C):
 def test_served_tokens_match_one_shot_oracle(dtype):
     shape, weights, X, m, xin = setup(dtype, n_layers=2, seed=3)
     ref = oracle_outputs(shape, weights, X)
-    for policy, C in [(S.POLICY_DECODE_MAXIMAL, 16), (S.POLICY_PREFILL_DECODE, 0)]:
-        got, res = serve_outputs(m, xin, policy, B=3, C=C)
+    for policy, C, kw in [(S.POLICY_DECODE_MAXIMAL, 16, {}), (S.POLICY_PREFILL_DECODE, 0, {}),
+                          (S.POLICY_MIXED, 0, dict(max_chunks=3, max_tokens=200))]:
+        got, res = serve_outputs(m, xin, policy, B=3, C=C, **kw)
         log(f"{serve.POLICY_NAMES[policy]} {dtype}: {res['iterations']} iterations "
             f"({res['hybrid_iterations']} hybrid)")
         for r, (p, d) in enumerate(REQS):
             e = rel_err(got[r, :p + d], ref[r])
             assert e <= TOL[dtype], (policy, r, e)
-        if policy == S.POLICY_DECODE_MAXIMAL:
+        if policy in (S.POLICY_DECODE_MAXIMAL, S.POLICY_MIXED):
             assert res["hybrid_iterations"] > 0
 
 

@@ -361,6 +361,43 @@ def test_concatenation_and_batch_invariance(kind):
         np.testing.assert_allclose(hyb.y[5 + b], alone.y[0], rtol=1e-12, atol=1e-13)
 
 
+def test_mixed_batch_equals_its_chunks_run_one_by_one():
+    """Mixed batching (several prompt chunks in one iteration, the baseline
+    mechanism of Sec. 5.2): every chunk's rows equal the same chunk run alone
+    as a prefill-only hybrid batch, the decodes equal a decode-only batch,
+    and a one-chunk mixed batch is the hybrid batch itself."""
+    shape = tiny_shape()
+    rng = np.random.default_rng(77)
+    w = rand_weights(shape, rng)
+    S = 32
+    cache = empty_cache(shape, 6, S)
+    chunks = [(2, 5, 4), (0, 0, 3), (5, 11, 6)]     # (slot, offset, length)
+    for slot, off, _ in chunks:
+        fill_prefix(cache, slot, off, rng)
+    ds, dc = [1, 4], [9, 0]
+    for slot, ctx in zip(ds, dc):
+        fill_prefix(cache, slot, ctx, rng)
+    x = rng.standard_normal((4 + 3 + 6 + 2, shape.hidden))
+    mix_cache = cache.copy()
+    mix = _run(shape, w, mix_cache, oracle.OracleMixedBatch(chunks, ds, dc), x)
+    ref_cache = cache.copy()
+    r0 = 0
+    for slot, off, n in chunks:
+        one = _run(shape, w, ref_cache, OracleBatch(slot, off, n, [], []), x[r0:r0 + n])
+        np.testing.assert_allclose(mix.y[r0:r0 + n], one.y, rtol=1e-12, atol=1e-13)
+        np.testing.assert_array_equal(mix.slots[r0:r0 + n], slot)
+        np.testing.assert_array_equal(mix.positions[r0:r0 + n], np.arange(off, off + n))
+        r0 += n
+    dec = _run(shape, w, ref_cache, OracleBatch(-1, 0, 0, ds, dc), x[r0:])
+    np.testing.assert_allclose(mix.y[r0:], dec.y, rtol=1e-12, atol=1e-13)
+    np.testing.assert_array_equal(np.isnan(mix_cache), np.isnan(ref_cache))
+    np.testing.assert_allclose(np.nan_to_num(mix_cache), np.nan_to_num(ref_cache), rtol=1e-12, atol=1e-13)
+    single = _run(shape, w, cache.copy(), oracle.OracleMixedBatch([chunks[0]], ds, dc),
+                  np.concatenate([x[:4], x[r0:]]))
+    hyb = _run(shape, w, cache.copy(), OracleBatch(2, 5, 4, ds, dc), np.concatenate([x[:4], x[r0:]]))
+    np.testing.assert_array_equal(single.y, hyb.y)
+
+
 def test_permuting_decodes_permutes_rows():
     shape = tiny_shape()
     w, cache, xc, xd, ds, dc = _hybrid_setup(shape, RNG)

@@ -198,6 +198,23 @@ class Batch:
 
 
 @dataclass
+class MixedBatch:
+    """Several prompt chunks plus decodes: chunks [(slot, offset, length)];
+    rows are chunk 0 in position order, chunk 1, ..., then the decodes."""
+    chunks: List[tuple]
+    decode_slots: np.ndarray
+    decode_ctx: np.ndarray
+
+    @property
+    def n_decodes(self) -> int:
+        return int(len(self.decode_slots))
+
+    @property
+    def n_tokens(self) -> int:
+        return sum(int(c[2]) for c in self.chunks) + self.n_decodes
+
+
+@dataclass
 class HostInstance:
     workload: Workload
     batch: Batch
@@ -222,10 +239,13 @@ def draw_batch(rng: np.random.Generator, spec: BatchSpec) -> Batch:
                  decode_slots=perm[1:1 + spec.n_decodes].copy(), decode_ctx=ctx)
 
 
-def valid_lengths(batch: Batch, n_slots: int) -> np.ndarray:
-    """Cached tokens per slot before the step (chunk slot: its offset)."""
+def valid_lengths(batch, n_slots: int) -> np.ndarray:
+    """Cached tokens per slot before the step (a chunk's slot: its offset)."""
     v = np.zeros(n_slots, dtype=np.int64)
-    if batch.chunk_len > 0:
+    if isinstance(batch, MixedBatch):
+        for s, o, _ in batch.chunks:
+            v[int(s)] = int(o)
+    elif batch.chunk_len > 0:
         v[batch.prefill_slot] = batch.chunk_offset
     for s, c in zip(batch.decode_slots, batch.decode_ctx):
         v[int(s)] = int(c)
@@ -274,9 +294,10 @@ def generate(w: Workload, n_layers: Optional[int] = None, batch: Optional[Batch]
     return HostInstance(workload=w, batch=b, x=x, kv=kv, weights=weights)
 
 
-def make_instance(shape: LayerShape, batch: Batch, max_seq_len: int, n_slots: int,
+def make_instance(shape: LayerShape, batch, max_seq_len: int, n_slots: int,
                   seed: int = 0, n_layers: int = 1, x_scale: float = 1.0) -> HostInstance:
-    """Instance for an explicitly given batch (tests of edge cases)."""
+    """Instance for an explicitly given batch (a Batch or a MixedBatch; tests
+    of edge cases)."""
     rng = np.random.Generator(np.random.PCG64(seed))
     T = batch.n_tokens
     x = _store(rng.standard_normal((T, shape.hidden), dtype=np.float32) * np.float32(x_scale), shape.dtype)
@@ -290,8 +311,9 @@ def make_instance(shape: LayerShape, batch: Batch, max_seq_len: int, n_slots: in
                 kv[layer, s, :, :, :n, :] = _store(
                     rng.standard_normal((2, nh, n, d), dtype=np.float32), shape.dtype)
     weights = [draw_weights(rng, shape) for _ in range(n_layers)]
-    spec = BatchSpec(chunk_len=batch.chunk_len, chunk_offset=batch.chunk_offset,
-                     prompt_len=batch.chunk_offset + batch.chunk_len, n_decodes=batch.n_decodes,
+    C = batch.n_tokens - batch.n_decodes
+    off = 0 if isinstance(batch, MixedBatch) else batch.chunk_offset
+    spec = BatchSpec(chunk_len=C, chunk_offset=off, prompt_len=off + C, n_decodes=batch.n_decodes,
                      ctx_lo=0, ctx_hi=0, max_seq_len=max_seq_len, n_slots=n_slots)
     wl = Workload(name="custom", shape=dataclasses.replace(shape, n_layers=n_layers), batch=spec, seed=seed)
     return HostInstance(workload=wl, batch=batch, x=x, kv=kv, weights=weights)
