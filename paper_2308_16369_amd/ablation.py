@@ -71,7 +71,8 @@ class LayerRunner:
     """One layer on the device, a KV cache of ``n_slots`` x ``max_seq_len``
     positions, and a workspace for up to ``max_tokens`` rows."""
 
-    def __init__(self, shape, n_slots: int, max_seq_len: int, max_tokens: int, max_decodes: int, seed: int = 0):
+    def __init__(self, shape, n_slots: int, max_seq_len: int, max_tokens: int, max_decodes: int, seed: int = 0,
+                 max_chunks: int = 1):
         import torch
 
         from workloads.stack import generate_layer_on_device
@@ -88,7 +89,7 @@ class LayerRunner:
         self.kv = S.sarathi_kv_alloc(self.cfg, n_slots, max_seq_len, kvt.data_ptr(),
                                      kvt.numel() * kvt.element_size())
         self.w = S.make_weights({k: t.data_ptr() for k, t in self.dev.weights.items()})
-        self.ws_bytes = S.sarathi_workspace_bytes(self.cfg, max_tokens, max_decodes, max_seq_len)
+        self.ws_bytes = S.sarathi_mixed_workspace_bytes(self.cfg, max_tokens, max_chunks, max_seq_len)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device="cuda")
         g = torch.Generator(device="cuda")
         g.manual_seed(seed + 1)
@@ -106,6 +107,16 @@ class LayerRunner:
         def launch(bb=bb, keep=keep):   # the closure keeps the host arrays alive
             S.sarathi_hybrid_layer_forward(self.cfg, self.w, self.kv, 0, bb, x.data_ptr(), y.data_ptr(),
                                            self.ws.data_ptr(), self.ws_bytes, self.stream.cuda_stream)
+        return launch
+
+    def call_mixed(self, chunks, decode_slots, decode_ctx) -> Callable[[], None]:
+        """A launcher of one layer call on a mixed batch: chunks [(slot, offset, length)]."""
+        mb, keep = self.S.make_mixed_batch(chunks, list(decode_slots), list(decode_ctx))
+        S, x, y = self.S, self.x, self.y
+
+        def launch(mb=mb, keep=keep):
+            S.sarathi_mixed_layer_forward(self.cfg, self.w, self.kv, 0, mb, x.data_ptr(), y.data_ptr(),
+                                          self.ws.data_ptr(), self.ws_bytes, self.stream.cuda_stream)
         return launch
 
     def time(self, calls: Sequence[Callable[[], None]], iters: int = 20, warmup: int = 3) -> float:
