@@ -275,7 +275,7 @@ int sarathi_mixed_model_step(const sarathi_model_cfg* cfg, const sarathi_layer_w
  * partials of the two residual kinds; with NULL or too small a buffer the op
  * runs without split-K (same result up to fp32 summation order, lower
  * occupancy at small M).  sarathi_linear_scratch_bytes(M, N) is the most it
- * can use (4 splits of M x N fp32).  Results are deterministic either way.
+ * can use (6 splits of M x N fp32).  Results are deterministic either way.
  */
 #define SARATHI_LINEAR_PLAIN        0
 #define SARATHI_LINEAR_RESID        1

@@ -341,8 +341,10 @@ static int cfg_bm(int cfg) {
 // Tile choice for the skinny matmuls of the hybrid batch (M = C + B rows).
 // Many W panels (>= 180 tiles of 128 rows) and M in (160, 320]: one block
 // covers all rows (W read once per block, 8 waves).  A middle count: 160-row
-// blocks.  Few panels (postproj / ffn_ln2 at N = hidden): 64-row blocks,
-// split-K below.  Small M: the block height that pads M least.
+// blocks.  Few panels (postproj / ffn_ln2 at N = hidden): 64-row blocks with
+// split-K -- or, when split-K scratch is available and M in (160, 320],
+// 320-row blocks split over K (chosen by the caller).  Small M: the block
+// height that pads M least.
 static int pick_cfg(int M, int n_panels) {
   if (M <= 64) return CFG_64x128;
   if (M <= 96) return CFG_96x128;
@@ -374,7 +376,8 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s) {
   constexpr int BN = 128;
   const int out_per_tile = (a.kind == LIN_SWIGLU) ? BN / 2 : BN;
   const int n_panels = (a.N + out_per_tile - 1) / out_per_tile;
-  const int cfg = pick_cfg(a.M, n_panels);
+  const bool split_kind = (a.kind == LIN_RESID || a.kind == LIN_RESID_F32IN) && a.parts != nullptr;
+  const int cfg = (split_kind && a.M > 160 && a.M <= 320 && n_panels < 256) ? CFG_320x128 : pick_cfg(a.M, n_panels);
   const int BM = cfg_bm(cfg);
   p.tiles_m = (a.M + BM - 1) / BM;
   p.tiles_n = n_panels;
@@ -389,13 +392,14 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s) {
   // Split-K for the residual ops when the tile grid leaves CUs idle: every
   // split stores its fp32 partial, then one pass adds residual + partials in
   // split order (deterministic).  Each split covers whole groups of two
-  // 64-wide k-tiles.
+  // 64-wide k-tiles.  With 320-row tiles (8 waves, one block per CU) the
+  // split count keeps the grid within one wave of blocks over the 256 CUs.
   const int tiles = p.tiles_m * p.tiles_n;
   const bool resid_kind = a.kind == LIN_RESID || a.kind == LIN_RESID_F32IN;
   int n_split = 1;
   if (resid_kind && a.parts != nullptr && tiles < 256) {
     const int kgroups = (a.K + 127) / 128;
-    int ns = (400 + tiles - 1) / tiles;
+    int ns = (cfg == CFG_320x128) ? 256 / tiles : (400 + tiles - 1) / tiles;
     if (ns > kgroups / 2) ns = kgroups / 2;
     if (ns > MAX_SPLIT) ns = MAX_SPLIT;
     if ((size_t)ns * a.M * a.N > a.parts_cap) ns = (int)(a.parts_cap / ((size_t)a.M * a.N));

@@ -47,7 +47,7 @@ struct LinearArgs {
   float* parts;         // residual kinds: fp32 scratch for split-K partials (null: no split-K)
   size_t parts_cap;     // its capacity in floats
 };
-constexpr int MAX_SPLIT = 4;   // split-K partials: at most MAX_SPLIT x [M, N] fp32
+constexpr int MAX_SPLIT = 6;   // split-K partials: at most MAX_SPLIT x [M, N] fp32
 hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s);
 
 // ---- attention

@@ -51,6 +51,8 @@ int hip_fail(hipError_t e, const char* what) {
 constexpr int SPLIT_KEYS = 256;   // keys per decode-attention work item
 constexpr int PRE_SPLIT = 256;    // keys per chunk-attention work item
 constexpr int QBLOCK = 64;        // chunk rows per chunk-attention work item
+constexpr int PARTS_ROWS = 512;   // split-K partials are sized for batches up to this many rows (larger
+                                  // batches fill the GPU without splitting; with less room fewer splits run)
 
 size_t esize(const sarathi_model_cfg* c) { return c->dtype == SARATHI_BF16 ? 2 : 4; }
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -101,7 +103,7 @@ Layout make_layout(const sarathi_model_cfg* c, int T, int n_chunks, int S) {
   L.o = take(T * QD * es);
   L.hres = take(T * H * 4);
   L.m = take(T * F * es);
-  L.parts = take((size_t)MAX_SPLIT * T * H * 4);
+  L.parts = take((size_t)MAX_SPLIT * std::min(T, PARTS_ROWS) * H * 4);
   // query blocks of 64 rows: each chunk starts a new block
   const size_t max_pre = ((size_t)(T + QBLOCK - 1) / QBLOCK + n_chunks - 1) * ((S + PRE_SPLIT - 1) / PRE_SPLIT);
   const size_t max_dec = (size_t)T * ((S + SPLIT_KEYS - 1) / SPLIT_KEYS);
@@ -324,7 +326,7 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
   const int* meta = reinterpret_cast<const int*>(ws + c.L.meta);
   float* hres = reinterpret_cast<float*>(ws + c.L.hres);
   float* parts = reinterpret_cast<float*>(ws + c.L.parts);
-  const size_t parts_cap = (size_t)MAX_SPLIT * T * H;
+  const size_t parts_cap = (size_t)MAX_SPLIT * std::min(T, PARTS_ROWS) * H;
   char* kv_layer = static_cast<char*>(c.kv->mem) + (size_t)layer * c.kv->st.layer * esize(cfg);
   hipError_t e;
   hipEvent_t* ev = prof_claim();

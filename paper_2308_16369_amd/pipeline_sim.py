@@ -131,7 +131,7 @@ def measure_cost_model(shape, max_seq: int = 4096, max_decodes: int = 32, log=la
     log("chunk attention fitted")
     Xd, yd = [], []
     rng = np.random.default_rng(0)
-    for B in [1, 4, 8, 16, max_decodes]:
+    for B in sorted({b for b in (1, 4, 8, 16, max_decodes) if b <= max_decodes}):
         for hi in sorted({h for h in (256, 1024, 2048, max_seq - 1) if h <= max_seq - 1}):
             ctx = rng.integers(max(0, hi // 4), hi, size=B)
             st = stages([r.call(Batch(-1, 0, 0, list(range(1, B + 1)), [int(c) for c in ctx]))])

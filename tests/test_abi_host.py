@@ -231,4 +231,4 @@ def test_linear_validation(lib):
                             check=False) == S.EINVAL                        # resid missing
     assert S.sarathi_linear(S.BF16, S.LINEAR_PLAIN, 0, 4, 16, FAKE_DEV, FAKE_DEV, 0, FAKE_DEV,
                             check=False) == S.EINVAL
-    assert S.sarathi_linear_scratch_bytes(320, 5120) == 4 * 320 * 5120 * 4
+    assert S.sarathi_linear_scratch_bytes(320, 5120) == 6 * 320 * 5120 * 4

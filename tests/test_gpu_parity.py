@@ -45,7 +45,8 @@ def run_and_check(inst: wl.HostInstance, label: str, layer: int = 0):
 
 # ============================================================================ linear ops
 
-LIN_SHAPES = [(72, 200, 264), (320, 640, 512), (283, 1000, 1032), (5, 17, 8), (544, 384, 256), (160, 128, 64)]
+LIN_SHAPES = [(72, 200, 264), (320, 640, 512), (283, 1000, 1032), (5, 17, 8), (544, 384, 256), (160, 128, 64),
+              (300, 5120, 2048)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
