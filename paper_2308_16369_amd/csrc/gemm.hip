@@ -1,16 +1,19 @@
 // Linear ops of the hybrid batch: one matmul over all C+B rows (Sec. 4.3,
 // "fuse all the linear operations"), y = x W^T with W stored [N, K].
 //
-// bf16: MFMA v_mfma_f32_16x16x32_bf16, 256 threads = 2x2 waves, block tile
-// BM x BN x 64, both operands staged through LDS (double-buffered, 16-byte
-// chunks XOR-swizzled by row so the MFMA operand reads are bank-conflict
-// free).  Both operands are K-contiguous, so every lane reads 16 contiguous
-// bytes for either MFMA operand.  Epilogues fuse the residual add
-// (postproj, ffn_ln2), SiLU*mul (SwiGLU ffn_ln1) and GELU.  Split-K stores
-// one fp32 partial per split; a separate pass adds residual + partials in a
-// fixed order, so results do not depend on scheduling.
+// bf16, K a multiple of 64 (every LLaMA / GPT-3 shape): gemm_ws_kernel, a
+// block of producer waves that move both operands from global memory into an
+// LDS ring with LDS DMA (global_load_lds_dwordx4) and consumer waves that run
+// v_mfma_f32_16x16x32_bf16 on LDS-staged tiles (16-byte chunks XOR-swizzled
+// by row so the operand reads are bank-conflict free).  Both operands are
+// K-contiguous, so every lane moves 16 contiguous bytes.  Epilogues fuse the
+// residual add (postproj, ffn_ln2), SiLU*mul (SwiGLU ffn_ln1) and GELU.
+// Split-K stores one fp32 partial per split; a separate pass adds residual +
+// partials in a fixed order, so results do not depend on scheduling.
 //
-// fp32: a plain LDS-tiled FMA kernel with the same epilogues.
+// bf16 with a ragged K: gemm_bf16_kernel, the same tiles loaded through
+// registers (k-chunks past K zeroed).  fp32: a plain LDS-tiled FMA kernel
+// with the same epilogues.
 #include "kernels.h"
 
 namespace sarathi {
@@ -45,7 +48,7 @@ __device__ __forceinline__ void epi_store(const GemmP& p, int r, int c, float v,
   }
 }
 
-// ============================================================================ bf16 MFMA
+// ============================================================================ bf16 MFMA, register-staged
 // Block tile BM x BN (W rows) x 64, WGM x WGN waves, PD register stages of
 // prefetch.  Loads are unconditional (addresses clamped into the operands) so
 // the compiler can keep PD tiles in flight with partial vmcnt waits; rows and
@@ -218,6 +221,184 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_kernel(GemmP p) {
   }
 }
 
+// ============================================================================ LDS DMA helpers
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// One wave instruction: lane i copies 16 bytes from src (its own address) to
+// dst + 16 i (dst is the same for the whole wave), global_load_lds_dwordx4.
+__device__ __forceinline__ void dma16(const void* src, uint4* dst) {
+  __builtin_amdgcn_global_load_lds(src, (lds_void_t*)dst, 16, 0, 0);
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  // gfx9 s_waitcnt: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] at [15:14]
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Workgroup barrier without the fence of __syncthreads(): the fence would
+// make the compiler wait for every outstanding LDS DMA load (vmcnt 0) and
+// drain the ring.  The memory clobber keeps LDS accesses on their side.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+// The same after this wave's LDS reads have returned, so a stage it has read
+// can be refilled by DMA once every wave has passed the barrier.
+__device__ __forceinline__ void lds_read_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// ============================================================================ bf16 MFMA, producer/consumer waves
+// The memory pipeline of a CU holds a bounded number of outstanding cache-line
+// requests, and a wave that issues a load while it is full stalls at the
+// issue.  When the same waves load and multiply, those stalls serialise the
+// operand feed with the MFMAs.  Here NP producer waves only issue LDS DMA
+// loads (and wait for them) while WGM x WGN consumer waves only read LDS and
+// run MFMAs; one barrier per k-tile hands a filled stage to the consumers
+// and the consumed stage back to the producers.  S-stage LDS ring, K a
+// multiple of 64.
+template <int EPI, int WTN>
+__device__ __forceinline__ int w_row_of(int nl, int n0_out, int N) {
+  if (EPI == EPI_SWIGLU) {
+    // each consumer wave's WTN columns: first half gate rows, second half up rows
+    const int q = nl / WTN, w = nl % WTN, half = WTN / 2;
+    const int jj = n0_out + q * half + (w % half);
+    return jj < N ? ((w < half) ? jj : N + jj) : 0;
+  }
+  return min(n0_out + nl, N - 1);
+}
+
+template <int BM, int BN, int WGM, int WGN, int NP, int S, int EPI>
+__global__ __launch_bounds__(64 * (WGM * WGN + NP)) void gemm_ws_kernel(GemmP p) {
+  constexpr int NC = WGM * WGN;
+  constexpr int BK = 64;
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;
+  constexpr int FM = WTM / 16, FN = WTN / 16;
+  constexpr int ROWS = BM + BN;
+  constexpr int G = ROWS / 8, GA = BM / 8;
+  constexpr int IHI = (G + NP - 1) / NP, ILO = G / NP, RHI = G % NP;
+  static_assert(BM % 8 == 0 && BN % 8 == 0 && ILO > 0, "8-row groups");
+  static_assert(WTM % 16 == 0 && WTN % 16 == 0 && (EPI != EPI_SWIGLU || FN % 2 == 0), "wave tile");
+  static_assert((S - 2) * IHI < 64 && S >= 2, "stages");
+  extern __shared__ uint4 lds[];                 // [S][ROWS * 8] 16-byte chunks
+
+  const int per = gridDim.x / 8;
+  const int t = (blockIdx.x % 8) * per + blockIdx.x / 8;
+  if (t >= p.n_tiles) return;
+  const int tile_m = t % p.tiles_m;
+  const int rest = t / p.tiles_m;
+  const int split = rest % p.n_split;
+  const int tile_n = rest / p.n_split;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int m0 = tile_m * BM;
+  const int n0_out = tile_n * (EPI == EPI_SWIGLU ? BN / 2 : BN);
+  const int kbeg = split * p.k_split;
+  const int kend = min(p.K, kbeg + p.k_split);
+  const int nk = (kend - kbeg) / BK;
+
+  if (wave >= NC) {
+    // ---------------- producer
+    const int q = wave - NC;
+    const bf16* A = reinterpret_cast<const bf16*>(p.A);
+    const bf16* W = reinterpret_cast<const bf16*>(p.W);
+    const int lchunk = (lane & 7) ^ (lane >> 3);
+    const bf16* src[IHI];
+#pragma unroll
+    for (int j = 0; j < IHI; ++j) {
+      const int g = min(j * NP + q, G - 1);
+      const int row = g * 8 + (lane >> 3);
+      const size_t r = g < GA ? (size_t)min(m0 + row, p.M - 1) : 0;
+      src[j] = g < GA ? A + r * p.K + kbeg + lchunk * 8
+                      : W + (size_t)w_row_of<EPI, WTN>(row - BM, n0_out, p.N) * p.K + kbeg + lchunk * 8;
+    }
+    const bool extra = q < RHI;
+    auto issue = [&](int stage, int kt) {
+      uint4* dst = lds + stage * ROWS * 8;
+#pragma unroll
+      for (int j = IHI - 1; j >= 0; --j)
+        if (j < ILO || extra) dma16(src[j] + (size_t)kt * BK, dst + (j * NP + q) * 64);
+    };
+    auto wait_next = [&](bool all) {   // all but the newest S - 2 stages landed
+      if (all) wait_vmcnt<0>();
+      else if (extra) wait_vmcnt<(S - 2) * IHI>();
+      else wait_vmcnt<(S - 2) * ILO>();
+    };
+#pragma unroll
+    for (int st = 0; st < S - 1; ++st)
+      if (st < nk) issue(st, st);
+    wait_next(S - 2 >= nk);
+    lds_barrier();
+    int nbuf = S - 1;
+    for (int kt = 0; kt < nk; ++kt) {
+      const bool more = kt + S - 1 < nk;
+      if (more) issue(nbuf, kt + S - 1);
+      wait_next(!more);
+      lds_barrier();
+      nbuf = (nbuf + 1 == S) ? 0 : nbuf + 1;
+    }
+    return;
+  }
+
+  // ---------------- consumer
+  const int wm = wave / WGN, wn = wave % WGN;
+  floatx4 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  lds_barrier();
+  int buf = 0;
+  for (int kt = 0; kt < nk; ++kt) {
+    const uint4* s = lds + buf * ROWS * 8;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const int ch = ks * 4 + (lane >> 4);
+      bf16x8_t af[FM], bfr[FN];
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm) {
+        const int r = wm * WTM + fm * 16 + (lane & 15);
+        af[fm] = __builtin_bit_cast(bf16x8_t, s[r * 8 + (ch ^ (r & 7))]);
+      }
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) {
+        const int r = BM + wn * WTN + fn * 16 + (lane & 15);
+        bfr[fn] = __builtin_bit_cast(bf16x8_t, s[r * 8 + (ch ^ (r & 7))]);
+      }
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn)
+          acc[fm][fn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[fm], bfr[fn], acc[fm][fn], 0, 0, 0);
+    }
+    lds_read_barrier();
+    buf = (buf + 1 == S) ? 0 : buf + 1;
+  }
+
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = m0 + wm * WTM + fm * 16 + 4 * (lane >> 4) + i;
+      if (r >= p.M) continue;
+      if (EPI == EPI_SWIGLU) {
+#pragma unroll
+        for (int fn = 0; fn < FN / 2; ++fn) {
+          const int c = n0_out + wn * (WTN / 2) + fn * 16 + (lane & 15);
+          if (c < p.N) {
+            const float v = silu_f(acc[fm][fn][i]) * acc[fm][fn + FN / 2][i];
+            reinterpret_cast<bf16*>(p.out)[(size_t)r * p.N + c] = f2bf(v);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn) {
+          const int c = n0_out + wn * WTN + fn * 16 + (lane & 15);
+          if (c < p.N) epi_store<bf16, EPI>(p, r, c, acc[fm][fn][i], split);
+        }
+      }
+    }
+  }
+}
+
 // ============================================================================ fp32 FMA
 // 64x64 tile of W rows (SwiGLU: 32 gate + 32 up rows -> 32 outputs), BK 16,
 // 16x16 threads with 4x4 results each.
@@ -309,6 +490,22 @@ static hipError_t run_bf16(GemmP p, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <int BM, int BN, int WGM, int WGN, int NP, int S, int EPI>
+static hipError_t run_ws(GemmP p, hipStream_t s) {
+  const size_t lds_bytes = (size_t)S * (BM + BN) * 8 * sizeof(uint4);
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute((const void*)gemm_ws_kernel<BM, BN, WGM, WGN, NP, S, EPI>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  const int grid = (p.n_tiles + 7) / 8 * 8;
+  hipLaunchKernelGGL((gemm_ws_kernel<BM, BN, WGM, WGN, NP, S, EPI>), dim3(grid), dim3(64 * (WGM * WGN + NP)),
+                     lds_bytes, s, p);
+  return hipGetLastError();
+}
+
 template <int BM, int BN, int WGM, int WGN, int PD>
 static hipError_t run_bf16_epi(int epi, const GemmP& p, hipStream_t s) {
   switch (epi) {
@@ -356,6 +553,49 @@ static int pick_cfg(int M, int n_panels) {
   return CFG_64x128;
 }
 
+// Producer/consumer tiles (BM x BN W rows; consumer waves 1 x 4 for BM = 64,
+// else 2 x 4; 4 producer waves) and their LDS ring depth (~120-156 KB).
+enum WsCfg { WS_64x128 = 0, WS_64x256, WS_96x128, WS_96x256, WS_160x128, WS_160x256 };
+
+template <int EPI>
+static hipError_t run_ws_cfg(int cfg, const GemmP& p, hipStream_t s) {
+  switch (cfg) {
+    case WS_64x128: return run_ws<64, 128, 1, 4, 4, 6, EPI>(p, s);
+    case WS_64x256: return run_ws<64, 256, 1, 4, 4, 3, EPI>(p, s);
+    case WS_96x128: return run_ws<96, 128, 2, 4, 4, 5, EPI>(p, s);
+    case WS_96x256: return run_ws<96, 256, 2, 4, 4, 3, EPI>(p, s);
+    case WS_160x128: return run_ws<160, 128, 2, 4, 4, 4, EPI>(p, s);
+    default: return run_ws<160, 256, 2, 4, 4, 3, EPI>(p, s);
+  }
+}
+
+static hipError_t run_ws_epi(int epi, int cfg, const GemmP& p, hipStream_t s) {
+  switch (epi) {
+    case EPI_STORE: return run_ws_cfg<EPI_STORE>(cfg, p, s);
+    case EPI_GELU: return run_ws_cfg<EPI_GELU>(cfg, p, s);
+    case EPI_SWIGLU: return run_ws_cfg<EPI_SWIGLU>(cfg, p, s);
+    case EPI_RESID_TO_F32: return run_ws_cfg<EPI_RESID_TO_F32>(cfg, p, s);
+    case EPI_RESIDF32_TO_ACT: return run_ws_cfg<EPI_RESIDF32_TO_ACT>(cfg, p, s);
+    default: return run_ws_cfg<EPI_PARTIAL>(cfg, p, s);
+  }
+}
+
+static int ws_bm(int cfg) { return cfg <= WS_64x256 ? 64 : (cfg <= WS_96x256 ? 96 : 160); }
+static int ws_bn(int cfg) { return (cfg == WS_64x256 || cfg == WS_96x256 || cfg == WS_160x256) ? 256 : 128; }
+
+// Each CU streams its tile's A rows (L2 hits) and W rows (mostly HBM) through
+// a bounded number of outstanding requests, so the operand feed per flop,
+// ~ 1/BN (A) + 2.3/BM (W), sets the speed: the tallest block that pads M
+// little, and 256 W rows per block when that still leaves >= 200 blocks (or
+// when split-K fills the GPU anyway).
+static int pick_ws(int M, int n_out, bool swiglu, bool split_ok) {
+  const int base = M <= 64 ? WS_64x128 : (M <= 96 ? WS_96x128 : WS_160x128);
+  const int bm = ws_bm(base);
+  const int tiles_m = (M + bm - 1) / bm;
+  const int panels256 = (n_out + (swiglu ? 127 : 255)) / (swiglu ? 128 : 256);
+  return (split_ok || tiles_m * panels256 >= 200) ? base + 1 : base;
+}
+
 hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
   GemmP p{};
@@ -373,14 +613,6 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s) {
     }
   }
 
-  constexpr int BN = 128;
-  const int out_per_tile = (a.kind == LIN_SWIGLU) ? BN / 2 : BN;
-  const int n_panels = (a.N + out_per_tile - 1) / out_per_tile;
-  const bool split_kind = (a.kind == LIN_RESID || a.kind == LIN_RESID_F32IN) && a.parts != nullptr;
-  const int cfg = (split_kind && a.M > 160 && a.M <= 320 && n_panels < 256) ? CFG_320x128 : pick_cfg(a.M, n_panels);
-  const int BM = cfg_bm(cfg);
-  p.tiles_m = (a.M + BM - 1) / BM;
-  p.tiles_n = n_panels;
   int epi;
   switch (a.kind) {
     case LIN_PLAIN: epi = EPI_STORE; break;
@@ -389,17 +621,36 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s) {
     case LIN_RESID: epi = EPI_RESID_TO_F32; break;
     default: epi = EPI_RESIDF32_TO_ACT; break;
   }
+  const bool swiglu = a.kind == LIN_SWIGLU;
+  const bool resid_kind = a.kind == LIN_RESID || a.kind == LIN_RESID_F32IN;
+  const bool ws = (a.K % 64) == 0;   // producer/consumer kernel: whole 64-wide k-tiles
+
+  int cfg, BM, BN;
+  if (ws) {
+    cfg = pick_ws(a.M, a.N, swiglu, resid_kind && a.parts != nullptr);
+    BM = ws_bm(cfg);
+    BN = ws_bn(cfg);
+  } else {
+    BN = 128;
+    const int n_panels = (a.N + (swiglu ? BN / 2 : BN) - 1) / (swiglu ? BN / 2 : BN);
+    const bool split_kind = resid_kind && a.parts != nullptr;
+    cfg = (split_kind && a.M > 160 && a.M <= 320 && n_panels < 256) ? CFG_320x128 : pick_cfg(a.M, n_panels);
+    BM = cfg_bm(cfg);
+  }
+  const int out_per_tile = swiglu ? BN / 2 : BN;
+  p.tiles_m = (a.M + BM - 1) / BM;
+  p.tiles_n = (a.N + out_per_tile - 1) / out_per_tile;
+
   // Split-K for the residual ops when the tile grid leaves CUs idle: every
   // split stores its fp32 partial, then one pass adds residual + partials in
   // split order (deterministic).  Each split covers whole groups of two
-  // 64-wide k-tiles.  With 320-row tiles (8 waves, one block per CU) the
-  // split count keeps the grid within one wave of blocks over the 256 CUs.
+  // 64-wide k-tiles.  Blocks of ~150 KB of LDS run one per CU, so the split
+  // count keeps the grid within one wave of blocks over the 256 CUs.
   const int tiles = p.tiles_m * p.tiles_n;
-  const bool resid_kind = a.kind == LIN_RESID || a.kind == LIN_RESID_F32IN;
   int n_split = 1;
   if (resid_kind && a.parts != nullptr && tiles < 256) {
     const int kgroups = (a.K + 127) / 128;
-    int ns = (cfg == CFG_320x128) ? 256 / tiles : (400 + tiles - 1) / tiles;
+    int ns = (ws || cfg == CFG_320x128) ? 256 / tiles : (400 + tiles - 1) / tiles;
     if (ns > kgroups / 2) ns = kgroups / 2;
     if (ns > MAX_SPLIT) ns = MAX_SPLIT;
     if ((size_t)ns * a.M * a.N > a.parts_cap) ns = (int)(a.parts_cap / ((size_t)a.M * a.N));
@@ -414,11 +665,15 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s) {
   }
   p.n_tiles = p.tiles_m * p.tiles_n * p.n_split;
   hipError_t e;
-  switch (cfg) {
-    case CFG_320x128: e = run_bf16_epi<320, 128, 4, 2, 2>(epi, p, s); break;
-    case CFG_64x128: e = run_bf16_epi<64, 128, 2, 2, 2>(epi, p, s); break;
-    case CFG_96x128: e = run_bf16_epi<96, 128, 2, 2, 2>(epi, p, s); break;
-    default: e = run_bf16_epi<160, 128, 2, 2, 2>(epi, p, s); break;
+  if (ws) {
+    e = run_ws_epi(epi, cfg, p, s);
+  } else {
+    switch (cfg) {
+      case CFG_320x128: e = run_bf16_epi<320, 128, 4, 2, 2>(epi, p, s); break;
+      case CFG_64x128: e = run_bf16_epi<64, 128, 2, 2, 2>(epi, p, s); break;
+      case CFG_96x128: e = run_bf16_epi<96, 128, 2, 2, 2>(epi, p, s); break;
+      default: e = run_bf16_epi<160, 128, 2, 2, 2>(epi, p, s); break;
+    }
   }
   if (e != hipSuccess) return e;
   if (n_split > 1)
