@@ -129,55 +129,71 @@ hipError_t launch_norm(int dtype, bool in_f32, bool layer_norm, const void* in, 
 }
 
 // ------------------------------------------------------------------ RoPE + KV append
-// Block: heads_per_block heads x (hd/2) threads; thread i rotates the pair
-// (i, i + hd/2) of q and k by angle pos * base^(-2i/hd) (angle in fp64), writes
-// q back in place and k, v to the cache at (slot, pos).
+// One thread per (row, head, group of P consecutive pair indices), P = 16
+// bytes of T: it rotates the pairs (i, i + hd/2), i in [i0, i0 + P), of q and
+// k by angle pos * base^(-2i/hd) (angle reduced in fp64, sin/cos in fp32),
+// writes q back in place and k, v to the cache at (slot, pos), all with
+// 16-byte accesses.
 template <typename T>
-__global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a, int heads_per_block) {
-  const int half = a.hd / 2;
-  const int h = blockIdx.y * heads_per_block + threadIdx.x / half;
-  const int i = threadIdx.x % half;
-  if (h >= a.nh) return;
-  const int row = blockIdx.x;
+__global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
+  constexpr int P = Vec16<T>::N;
+  const int half = a.hd / 2, groups = half / P;
+  const size_t t = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
+  if (t >= (size_t)a.T * a.nh * groups) return;
+  const int grp = (int)(t % groups);
+  const int h = (int)((t / groups) % a.nh);
+  const int row = (int)(t / ((size_t)groups * a.nh));
+  const int i0 = grp * P;
   const int slot = a.row_slot[row];
   const int pos = a.row_pos[row];
   T* base = reinterpret_cast<T*>(a.qkv) + (size_t)row * (3 * a.nh * a.hd);
   T* q = base + h * a.hd;
-  T* k = base + a.nh * a.hd + h * a.hd;
+  const T* k = base + a.nh * a.hd + h * a.hd;
   const T* v = base + 2 * a.nh * a.hd + h * a.hd;
-  float q0 = to_f<T>(q[i]), q1 = to_f<T>(q[i + half]);
-  float k0 = to_f<T>(k[i]), k1 = to_f<T>(k[i + half]);
-  if (a.rope) {
+  T* cache = reinterpret_cast<T*>(a.kv_layer);
+  T* kd = cache + (size_t)slot * a.st.slot + (size_t)h * a.st.head + (size_t)pos * a.st.pos;
+  T* vd = kd + a.st.kv;
+  const uint4 k_lo = *reinterpret_cast<const uint4*>(k + i0), k_hi = *reinterpret_cast<const uint4*>(k + half + i0);
+  *reinterpret_cast<uint4*>(vd + i0) = *reinterpret_cast<const uint4*>(v + i0);
+  *reinterpret_cast<uint4*>(vd + half + i0) = *reinterpret_cast<const uint4*>(v + half + i0);
+  if (!a.rope) {
+    *reinterpret_cast<uint4*>(kd + i0) = k_lo;
+    *reinterpret_cast<uint4*>(kd + half + i0) = k_hi;
+    return;
+  }
+  float q0[P], q1[P], k0[P], k1[P];
+  Vec16<T>::unpack(*reinterpret_cast<const uint4*>(q + i0), q0);
+  Vec16<T>::unpack(*reinterpret_cast<const uint4*>(q + half + i0), q1);
+  Vec16<T>::unpack(k_lo, k0);
+  Vec16<T>::unpack(k_hi, k1);
+  const double lb = log2((double)a.base);
+#pragma unroll
+  for (int e = 0; e < P; ++e) {
     // angle pos * base^(-2i/hd), reduced to [-pi, pi] in fp64, sin/cos in fp32
-    const double theta = exp2(-2.0 * (double)i / (double)a.hd * log2((double)a.base));
+    const double theta = exp2(-2.0 * (double)(i0 + e) / (double)a.hd * lb);
     const double ang = (double)pos * theta;
     const double red = ang - 6.283185307179586 * rint(ang * 0.15915494309189535);
     float sn, c;
     __sincosf((float)red, &sn, &c);
-    const float nq0 = q0 * c - q1 * sn, nq1 = q0 * sn + q1 * c;
-    const float nk0 = k0 * c - k1 * sn, nk1 = k0 * sn + k1 * c;
-    q0 = nq0; q1 = nq1; k0 = nk0; k1 = nk1;
-    q[i] = from_f<T>(q0);
-    q[i + half] = from_f<T>(q1);
+    const float nq0 = q0[e] * c - q1[e] * sn, nq1 = q0[e] * sn + q1[e] * c;
+    const float nk0 = k0[e] * c - k1[e] * sn, nk1 = k0[e] * sn + k1[e] * c;
+    q0[e] = nq0; q1[e] = nq1; k0[e] = nk0; k1[e] = nk1;
   }
-  T* cache = reinterpret_cast<T*>(a.kv_layer);
-  T* kd = cache + (size_t)slot * a.st.slot + (size_t)h * a.st.head + (size_t)pos * a.st.pos;
-  T* vd = kd + a.st.kv;
-  kd[i] = from_f<T>(k0);
-  kd[i + half] = from_f<T>(k1);
-  vd[i] = v[i];
-  vd[i + half] = v[i + half];
+  *reinterpret_cast<uint4*>(q + i0) = Store16<T>::pack(q0);
+  *reinterpret_cast<uint4*>(q + half + i0) = Store16<T>::pack(q1);
+  *reinterpret_cast<uint4*>(kd + i0) = Store16<T>::pack(k0);
+  *reinterpret_cast<uint4*>(kd + half + i0) = Store16<T>::pack(k1);
 }
 
 hipError_t launch_rope_append(int dtype, const RopeArgs& a, hipStream_t s) {
   if (a.T <= 0) return hipSuccess;
-  const int half = a.hd / 2;
-  const int hpb = 256 / half;
-  dim3 grid(a.T, (a.nh + hpb - 1) / hpb);
+  const int P = dtype == 0 ? 4 : 8;   // pairs per thread (16 bytes)
+  const size_t threads = (size_t)a.T * a.nh * (a.hd / 2 / P);
+  const dim3 grid((unsigned)((threads + 255) / 256));
   if (dtype == 0)
-    hipLaunchKernelGGL(rope_append_kernel<float>, grid, dim3(hpb * half), 0, s, a, hpb);
+    hipLaunchKernelGGL(rope_append_kernel<float>, grid, dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL(rope_append_kernel<bf16>, grid, dim3(hpb * half), 0, s, a, hpb);
+    hipLaunchKernelGGL(rope_append_kernel<bf16>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -194,9 +210,9 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const Tr* __restrict_
     for (int e = 0; e < V; ++e) acc[e] = to_f<Tr>(resid[i * V + e]);
     for (int sp = 0; sp < n_split; ++sp) {
       const float* pp = parts + (size_t)sp * n + i * V;
-      if (V == 4) {
+      if constexpr (V == 4) {
         const float4 q = *reinterpret_cast<const float4*>(pp);
-        acc[0] += q.x; acc[1] += q.y; acc[2] += q.z; acc[V - 1] += q.w;
+        acc[0] += q.x; acc[1] += q.y; acc[2] += q.z; acc[3] += q.w;
       } else {
 #pragma unroll
         for (int e = 0; e < V; ++e) acc[e] += pp[e];
