@@ -553,15 +553,16 @@ static int pick_cfg(int M, int n_panels) {
   return CFG_64x128;
 }
 
-// Producer/consumer tiles (BM x BN W rows; consumer waves 1 x 4 for BM = 64,
-// else 2 x 4; 4 producer waves) and their LDS ring depth (~120-156 KB).
-enum WsCfg { WS_64x128 = 0, WS_64x256, WS_96x128, WS_96x256, WS_160x128, WS_160x256 };
+// Producer/consumer tiles (BM x BN W rows; consumer waves 2 x 4, or 2 x 2
+// for BN = 64; 4 producer waves) and their LDS ring depth (~100-156 KB).
+enum WsCfg { WS_64x64 = 0, WS_64x128, WS_64x256, WS_96x128, WS_96x256, WS_160x128, WS_160x256 };
 
 template <int EPI>
 static hipError_t run_ws_cfg(int cfg, const GemmP& p, hipStream_t s) {
   switch (cfg) {
-    case WS_64x128: return run_ws<64, 128, 1, 4, 4, 6, EPI>(p, s);
-    case WS_64x256: return run_ws<64, 256, 1, 4, 4, 3, EPI>(p, s);
+    case WS_64x64: return run_ws<64, 64, 2, 2, 4, 6, EPI>(p, s);
+    case WS_64x128: return run_ws<64, 128, 2, 4, 4, 6, EPI>(p, s);
+    case WS_64x256: return run_ws<64, 256, 2, 4, 4, 3, EPI>(p, s);
     case WS_96x128: return run_ws<96, 128, 2, 4, 4, 5, EPI>(p, s);
     case WS_96x256: return run_ws<96, 256, 2, 4, 4, 3, EPI>(p, s);
     case WS_160x128: return run_ws<160, 128, 2, 4, 4, 4, EPI>(p, s);
@@ -581,19 +582,30 @@ static hipError_t run_ws_epi(int epi, int cfg, const GemmP& p, hipStream_t s) {
 }
 
 static int ws_bm(int cfg) { return cfg <= WS_64x256 ? 64 : (cfg <= WS_96x256 ? 96 : 160); }
-static int ws_bn(int cfg) { return (cfg == WS_64x256 || cfg == WS_96x256 || cfg == WS_160x256) ? 256 : 128; }
+static int ws_bn(int cfg) {
+  return cfg == WS_64x64 ? 64 : ((cfg == WS_64x256 || cfg == WS_96x256 || cfg == WS_160x256) ? 256 : 128);
+}
 
-// Each CU streams its tile's A rows (L2 hits) and W rows (mostly HBM) through
-// a bounded number of outstanding requests, so the operand feed per flop,
-// ~ 1/BN (A) + 2.3/BM (W), sets the speed: the tallest block that pads M
-// little, and 256 W rows per block when that still leaves >= 200 blocks (or
-// when split-K fills the GPU anyway).
+// A CU's operand feed is bounded by its outstanding memory requests, so the
+// tile shape sets the speed: the tallest block that pads M little (fewer W
+// re-reads), then the widest block (fewer A re-reads) that still leaves
+// >= 200 blocks for the 256 CUs.  The split-K ops fill the GPU through their
+// splits: 256 W rows for 160-row blocks, 128 for shorter ones.
 static int pick_ws(int M, int n_out, bool swiglu, bool split_ok) {
-  const int base = M <= 64 ? WS_64x128 : (M <= 96 ? WS_96x128 : WS_160x128);
-  const int bm = ws_bm(base);
+  const int bm = M <= 64 ? 64 : (M <= 96 ? 96 : 160);
   const int tiles_m = (M + bm - 1) / bm;
-  const int panels256 = (n_out + (swiglu ? 127 : 255)) / (swiglu ? 128 : 256);
-  return (split_ok || tiles_m * panels256 >= 200) ? base + 1 : base;
+  auto tiles = [&](int bn) {
+    const int per = swiglu ? bn / 2 : bn;
+    return tiles_m * ((n_out + per - 1) / per);
+  };
+  int bn;
+  if (split_ok) bn = bm == 160 ? 256 : 128;
+  else if (tiles(256) >= 200) bn = 256;
+  else if (tiles(128) >= 200 || bm != 64) bn = 128;
+  else bn = 64;
+  if (bm == 64) return bn == 64 ? WS_64x64 : (bn == 128 ? WS_64x128 : WS_64x256);
+  if (bm == 96) return bn == 256 ? WS_96x256 : WS_96x128;
+  return bn == 256 ? WS_160x256 : WS_160x128;
 }
 
 hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s) {
