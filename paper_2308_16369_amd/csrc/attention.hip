@@ -5,11 +5,11 @@
 // Chunked-prefill attention (bf16, MFMA): the chunk's queries at positions
 // off..off+C-1 attend to the prefill slot's keys 0..position (the earlier
 // chunks' cached keys plus, causally, the chunk's own; Sec. 4.2).  Work item
-// = (64-query block, split of split_keys keys), one head per block of 4
-// waves x 16 query rows.  K and V tiles of 64 keys are staged in LDS (V
-// transposed so P*V reads 16 contiguous bytes per lane), the next tile is
-// prefetched into registers while the current one is used; S = Q K^T and
-// O += P V run on v_mfma_f32_16x16x32_bf16 with an fp32 online softmax.
+// = (block of PREFILL_QBLOCK queries, split of split_keys keys), one head per
+// block of PREFILL_QBLOCK / 16 waves x 16 query rows.  K and V tiles of 64
+// keys are staged in a ring of LDS stages by LDS DMA (V read back transposed
+// so P*V takes 16 contiguous bytes per lane); S = Q K^T and O += P V run on
+// v_mfma_f32_16x16x32_bf16 with an fp32 online softmax.
 //
 // Row attention (decodes; in fp32 runs also the chunk rows): each row attends
 // to keys 0..pos of its slot.  Work item = (row, split of split_keys keys); a
@@ -27,6 +27,13 @@ constexpr float LOG2E = 1.4426950408889634f;
 // ============================================================================ prefill (bf16, MFMA)
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 
+// Two fp32 -> one dword of two bf16 (round to nearest even; low half = a).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
+}
+
 // LDS transpose read (gfx950): within each group of 16 lanes, output lane j
 // element e is element (j % 4) of the 8 bytes addressed by lane 4e + j / 4.
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
@@ -35,8 +42,8 @@ __device__ __forceinline__ uint2 lds_read_tr16(const void* p) {
   return __builtin_bit_cast(uint2, v);
 }
 
-// One block = one head x (64 queries of the chunk, one split of keys); wave w
-// owns queries w*16..w*16+15.  Per 64-key tile:
+// One block = one head x (16 * NW queries of the chunk, one split of keys);
+// wave w owns queries w*16..w*16+15.  Per 64-key tile:
 //   S^T = K Q^T  (MFMA: A = K rows from LDS, B = the wave's Q fragments), so
 //     each lane holds 16 scores of ONE query (lane % 16) for keys
 //     nt*16 + 4*(lane/16) + i;
@@ -47,22 +54,31 @@ __device__ __forceinline__ uint2 lds_read_tr16(const void* p) {
 //     permutation of the 32 keys of a block: lane group g holds keys
 //     4g..4g+3 and 16+4g..16+4g+3, which is what two transpose reads of rows
 //     4g..4g+3 and 16+4g..16+4g+3 deliver.
-// K and V tiles are stored row-major (16-byte chunks XOR-swizzled by row),
-// double-buffered in LDS; the next tile is prefetched into registers while the
-// current one is used; one barrier per tile.
-template <int D>
-__global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(PrefillArgs a, float scale_log2) {
+// K and V tiles are stored row-major (16-byte chunks XOR-swizzled by row) in
+// an S-stage LDS ring filled by LDS DMA (global_load_lds_dwordx4: a wave
+// instruction fills 1 KB = 1024 / (2 D) key rows; lane i takes LDS slot i of
+// its row and so reads the chunk that the swizzle puts there), S - 1 tiles in
+// flight while one is used; one barrier per tile.
+template <int D, int NW, int S>
+__global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(PrefillArgs a, float scale_log2) {
+  constexpr int QB = 16 * NW;            // the block's queries (chunk rows)
   constexpr int KT = 64;                 // keys per tile
   constexpr int DCH = D / 8;             // 16-byte chunks per K/V row
-  constexpr int LD = KT * DCH / 256;     // chunks of K (and of V) per thread per tile
-  __shared__ u32x4 ks_[2][KT * DCH];     // K tile [key][D], chunk ^ (key & 7)
-  __shared__ u32x4 vs_[2][KT * DCH];     // V tile [key][D], chunk ^ (key & 7)
+  constexpr int TILE = KT * DCH;         // 16-byte chunks per K (or V) tile
+  constexpr int RPI = 64 / DCH;          // key rows per 1 KB DMA instruction
+  constexpr int GRP = 2 * KT / RPI;      // 1 KB groups per K+V tile pair
+  constexpr int NI = GRP / NW;           // DMA instructions per wave per tile
+  static_assert(NI * NW == GRP && (S - 2) * NI < 64 && S >= 2, "tile DMA split");
+  extern __shared__ u32x4 ring[];        // [S][K tile, V tile]
 
-  const int item = blockIdx.x, h = blockIdx.y;
-  const int* ch = a.chunks + 4 * a.work[2 * item];
+  const int per = gridDim.x / 8;
+  const int t = (blockIdx.x % 8) * per + blockIdx.x / 8;
+  if (t >= a.n_work * a.nh) return;
+  const int item = t % a.n_work, h = t / a.n_work;
+  const int* wk = a.work + 3 * item;
+  const int* ch = a.chunks + 4 * wk[0];
   const int slot = ch[0], offset = ch[1], C = ch[2], row0 = ch[3];
-  const int wv = a.work[2 * item + 1];
-  const int q0 = (wv >> 12) * 64, ksplit = wv & 4095;
+  const int q0 = (wk[1] >> 12) * QB, ksplit = wk[1] & 4095, pslot = wk[2];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int grp = lane >> 4, ql = lane & 15;
   const bf16* qkv = reinterpret_cast<const bf16*>(a.qkv) + (size_t)row0 * a.ld_qkv;
@@ -70,8 +86,8 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(PrefillArgs a, f
   const bf16* kbase = cache + (size_t)slot * a.st.slot + (size_t)h * a.st.head;
   const bf16* vbase = kbase + a.st.kv;
 
-  // This item's keys: [kbeg, kend) within 0 .. off + min(q0 + 64, C) - 1.
-  const int n_keys = offset + min(q0 + 64, C);
+  // This item's keys: [kbeg, kend) within 0 .. off + min(q0 + QB, C) - 1.
+  const int n_keys = offset + min(q0 + QB, C);
   const int kbeg = ksplit * a.split_keys;
   const int kend = min(n_keys, kbeg + a.split_keys);
   const int n_tiles = (kend - kbeg + KT - 1) / KT;
@@ -91,27 +107,25 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(PrefillArgs a, f
 #pragma unroll
   for (int dt = 0; dt < D / 16; ++dt) o_acc[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  // Tile loads into registers; key addresses are clamped to the item's last
-  // key (finite data; such keys are masked out of the softmax).
-  u32x4 kreg[LD], vreg[LD];
-  auto gload = [&](int kt) {
+  // Tile DMA: instruction j of wave w fills 1 KB group g = j * NW + w of the
+  // tile pair (K groups first, then V).  Key addresses are clamped to the
+  // item's last key (finite data; such keys are masked out of the softmax).
+  const int lrow = lane / DCH, lslot = lane % DCH;
+  const bf16* dsrc[NI];
+  int drow[NI];
+#pragma unroll
+  for (int j = 0; j < NI; ++j) {
+    const int g = j * NW + wave;
+    const int kv = g / (KT / RPI), row = (g % (KT / RPI)) * RPI + lrow;
+    drow[j] = row;
+    dsrc[j] = (kv ? vbase : kbase) + (lslot ^ (row & 7)) * 8;
+  }
+  auto issue = [&](int stage, int kt) {
     const int k0 = kbeg + kt * KT;
+    uint4* dst = reinterpret_cast<uint4*>(ring + stage * 2 * TILE);
 #pragma unroll
-    for (int j = 0; j < LD; ++j) {
-      const int c = tid + 256 * j;
-      const size_t off = (size_t)min(k0 + c / DCH, kend - 1) * a.st.pos + (c % DCH) * 8;
-      kreg[j] = *reinterpret_cast<const u32x4*>(kbase + off);
-      vreg[j] = *reinterpret_cast<const u32x4*>(vbase + off);
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int j = 0; j < LD; ++j) {
-      const int c = tid + 256 * j;
-      const int key = c / DCH, ch = c % DCH;
-      ks_[buf][key * DCH + (ch ^ (key & 7))] = kreg[j];
-      vs_[buf][key * DCH + (ch ^ (key & 7))] = vreg[j];
-    }
+    for (int j = 0; j < NI; ++j)
+      dma16(dsrc[j] + (size_t)min(k0 + drow[j], kend - 1) * a.st.pos, dst + (j * NW + wave) * 64);
   };
 
   // Transpose-read addressing of V^T fragments: lane i of group grp reads 8
@@ -121,18 +135,20 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(PrefillArgs a, f
   const int tr_c16 = (ql & 3) >> 1;      // 16-byte chunk within the 16 columns of dt
   const int tr_half = (ql & 1) * 8;      // byte offset inside the chunk
 
-  if (n_tiles > 0) {
-    gload(0);
-    sstore(0);
-  }
-  __syncthreads();
+#pragma unroll
+  for (int st = 0; st < S - 1; ++st)
+    if (st < n_tiles) issue(st, st);
+  int buf = 0, nbuf = S - 1;
   for (int kt = 0; kt < n_tiles; ++kt) {
-    const int buf = kt & 1;
     const int k0 = kbeg + kt * KT;
-    if (kt + 1 < n_tiles) gload(kt + 1);
-    // keep the next tile's loads in flight across this tile's work: the
-    // scheduler would otherwise hoist the LDS stores (and their waits) up here
-    __builtin_amdgcn_sched_barrier(0);
+    if (kt + S - 2 < n_tiles) wait_vmcnt<(S - 2) * NI>();
+    else wait_vmcnt<0>();
+    lds_read_barrier();
+    if (kt + S - 1 < n_tiles) issue(nbuf, kt + S - 1);
+    const u32x4* ks_ = ring + buf * 2 * TILE;
+    const u32x4* vs_ = ks_ + TILE;
+    buf = (buf + 1 == S) ? 0 : buf + 1;
+    nbuf = (nbuf + 1 == S) ? 0 : nbuf + 1;
 
     // ---- S^T = K Q^T: s[nt][i] = score of key k0 + nt*16 + 4*grp + i for query ql.
     floatx4 s[KT / 16];
@@ -143,51 +159,58 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(PrefillArgs a, f
 #pragma unroll
       for (int ks = 0; ks < D / 32; ++ks) {
         const int ch = ks * 4 + grp;
-        const bf16x8_t kf = __builtin_bit_cast(bf16x8_t, ks_[buf][key * DCH + (ch ^ (key & 7))]);
+        const bf16x8_t kf = __builtin_bit_cast(bf16x8_t, ks_[key * DCH + (ch ^ (key & 7))]);
         s[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, __builtin_bit_cast(bf16x8_t, qf[ks]), s[nt], 0, 0, 0);
       }
     }
 
-    // ---- mask (key position <= query position, key inside the item), online softmax.
+    // ---- online softmax (log2 units).  Keys past the query's position or the
+    // item's end are masked; a tile entirely before every query of the wave
+    // and inside the item needs no mask.
+    const bool full = k0 + KT <= kend && k0 + KT - 1 <= offset + q0 + wave * 16;
+    if (!full) {
+#pragma unroll
+      for (int nt = 0; nt < KT / 16; ++nt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int kp = k0 + nt * 16 + 4 * grp + i;
+          if (!(kp <= qpos && kp < kend)) s[nt][i] = -INFINITY;
+        }
+    }
     float mx = -INFINITY;
 #pragma unroll
     for (int nt = 0; nt < KT / 16; ++nt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int kp = k0 + nt * 16 + 4 * grp + i;
-        const float v = (kp <= qpos && kp < kend) ? s[nt][i] * scale_log2 : -INFINITY;
-        s[nt][i] = v;
-        mx = fmaxf(mx, v);
-      }
+      for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[nt][i]);
     mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
+    const float m_new = fmaxf(m_run, mx * scale_log2);
     const float m_safe = (m_new == -INFINITY) ? 0.f : m_new;
-    const float corr = exp2f(m_run - m_safe);
+    const float corr = __builtin_amdgcn_exp2f(m_run - m_safe);
     float sum = 0.f;
 #pragma unroll
     for (int nt = 0; nt < KT / 16; ++nt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        s[nt][i] = exp2f(s[nt][i] - m_safe);
+        s[nt][i] = __builtin_amdgcn_exp2f(fmaf(s[nt][i], scale_log2, -m_safe));
         sum += s[nt][i];
       }
     sum += __shfl_xor(sum, 16, 64);
     sum += __shfl_xor(sum, 32, 64);
     l_run = l_run * corr + sum;
     m_run = m_new;
+    if (__ballot(corr != 1.0f)) {
 #pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt) o_acc[dt] *= corr;
+      for (int dt = 0; dt < D / 16; ++dt) o_acc[dt] *= corr;
+    }
 
     // ---- O^T += V^T P^T over two 32-key blocks.
-    const char* vb = reinterpret_cast<const char*>(vs_[buf]);
+    const char* vb = reinterpret_cast<const char*>(vs_);
 #pragma unroll
     for (int kk = 0; kk < KT / 32; ++kk) {
-      u32x4 pw;
-      pw.x = (uint32_t)f2bf(s[2 * kk][0]) | ((uint32_t)f2bf(s[2 * kk][1]) << 16);
-      pw.y = (uint32_t)f2bf(s[2 * kk][2]) | ((uint32_t)f2bf(s[2 * kk][3]) << 16);
-      pw.z = (uint32_t)f2bf(s[2 * kk + 1][0]) | ((uint32_t)f2bf(s[2 * kk + 1][1]) << 16);
-      pw.w = (uint32_t)f2bf(s[2 * kk + 1][2]) | ((uint32_t)f2bf(s[2 * kk + 1][3]) << 16);
+      // probabilities to bf16 (round to nearest even, v_cvt_pk_bf16_f32)
+      const u32x4 pw{pack_bf16x2(s[2 * kk][0], s[2 * kk][1]), pack_bf16x2(s[2 * kk][2], s[2 * kk][3]),
+                     pack_bf16x2(s[2 * kk + 1][0], s[2 * kk + 1][1]), pack_bf16x2(s[2 * kk + 1][2], s[2 * kk + 1][3])};
       const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, pw);
       const int r0 = kk * 32 + tr_row, r1 = r0 + 16;
 #pragma unroll
@@ -199,15 +222,12 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(PrefillArgs a, f
         o_acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o_acc[dt], 0, 0, 0);
       }
     }
-    __builtin_amdgcn_sched_barrier(0);
-    if (kt + 1 < n_tiles) sstore(buf ^ 1);
-    __syncthreads();
   }
 
   // ---- partial of the lane's query (rows < C): [m, l, o[D]].
   const int rb = wave * 16 + ql;
   if (q0 + rb < C) {
-    float* dst = a.part + ((size_t)(item * 64 + rb) * a.nh + h) * (D + 2);
+    float* dst = a.part + ((size_t)(pslot * QB + rb) * a.nh + h) * (D + 2);
     if (grp == 0) {
       dst[0] = m_run;
       dst[1] = l_run;
@@ -219,16 +239,29 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(PrefillArgs a, f
   }
 }
 
+template <int D, int NW, int S>
+static hipError_t run_prefill(const PrefillArgs& a, unsigned grid, float scale_log2, hipStream_t s) {
+  const size_t lds_bytes = (size_t)S * 2 * 64 * (D / 8) * 16;
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute((const void*)attn_prefill_bf16_kernel<D, NW, S>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL((attn_prefill_bf16_kernel<D, NW, S>), dim3(grid), dim3(64 * NW), lds_bytes, s, a, scale_log2);
+  return hipGetLastError();
+}
+
 hipError_t launch_attn_prefill(int dtype, const PrefillArgs& a, hipStream_t s) {
   if (a.n_work <= 0) return hipSuccess;
   if (dtype != 1) return hipErrorInvalidValue;
   const float scale_log2 = LOG2E / sqrtf((float)a.hd);
-  dim3 grid(a.n_work, a.nh);
-  if (a.hd == 128)
-    hipLaunchKernelGGL(attn_prefill_bf16_kernel<128>, grid, dim3(256), 0, s, a, scale_log2);
-  else
-    hipLaunchKernelGGL(attn_prefill_bf16_kernel<64>, grid, dim3(256), 0, s, a, scale_log2);
-  return hipGetLastError();
+  const unsigned grid = (unsigned)(((size_t)a.n_work * a.nh + 7) / 8 * 8);
+  constexpr int NW = PREFILL_QBLOCK / 16;
+  // two stages (64 KB for head_dim 128): two blocks per CU
+  if (a.hd == 128) return run_prefill<128, NW, 2>(a, grid, scale_log2, s);
+  return run_prefill<64, NW, 2>(a, grid, scale_log2, s);
 }
 
 // ============================================================================ row attention

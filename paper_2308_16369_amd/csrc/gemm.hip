@@ -221,30 +221,6 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_kernel(GemmP p) {
   }
 }
 
-// ============================================================================ LDS DMA helpers
-typedef __attribute__((address_space(3))) void lds_void_t;
-
-// One wave instruction: lane i copies 16 bytes from src (its own address) to
-// dst + 16 i (dst is the same for the whole wave), global_load_lds_dwordx4.
-__device__ __forceinline__ void dma16(const void* src, uint4* dst) {
-  __builtin_amdgcn_global_load_lds(src, (lds_void_t*)dst, 16, 0, 0);
-}
-
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  // gfx9 s_waitcnt: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] at [15:14]
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
-
-// Workgroup barrier without the fence of __syncthreads(): the fence would
-// make the compiler wait for every outstanding LDS DMA load (vmcnt 0) and
-// drain the ring.  The memory clobber keeps LDS accesses on their side.
-__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
-// The same after this wave's LDS reads have returned, so a stage it has read
-// can be refilled by DMA once every wave has passed the barrier.
-__device__ __forceinline__ void lds_read_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
-
 // ============================================================================ bf16 MFMA, producer/consumer waves
 // The memory pipeline of a CU holds a bounded number of outstanding cache-line
 // requests, and a wave that issues a load while it is full stalls at the

@@ -54,6 +54,7 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s);
 // Partial results (one per row x head x key split): [m, l, o[hd]] in fp32,
 // m the running max of the log2-scaled scores, l the sum of 2^(s - m),
 // o the unnormalised weighted sum of values.
+constexpr int PREFILL_QBLOCK = 128;   // chunk rows per chunk-attention work item
 struct PrefillArgs {
   const void* qkv;      // all rows; chunk c's rows start at its first-row entry; q columns rotated
   int ld_qkv;
@@ -61,9 +62,9 @@ struct PrefillArgs {
   KVStrides st;
   const int* chunks;    // [n_chunks][slot, offset, len, first row]
   int nh, hd;
-  const int* work;      // [n_work][chunk, (q_block << 12) | key_split]
+  const int* work;      // [n_work][chunk, (q_block << 12) | key_split, partial slot p]
   int n_work, split_keys;
-  float* part;          // item i, row j of its q-block -> partial index i * 64 + j
+  float* part;          // row j of an item's q-block -> partial index p * PREFILL_QBLOCK + j
 };
 hipError_t launch_attn_prefill(int dtype, const PrefillArgs& a, hipStream_t s);
 

@@ -49,8 +49,8 @@ int hip_fail(hipError_t e, const char* what) {
 }
 
 constexpr int SPLIT_KEYS = 256;   // keys per decode-attention work item
-constexpr int PRE_SPLIT = 256;    // keys per chunk-attention work item
-constexpr int QBLOCK = 64;        // chunk rows per chunk-attention work item
+constexpr int PRE_SPLIT = 256;    // smallest key split of a chunk-attention work item
+constexpr int QBLOCK = PREFILL_QBLOCK;   // chunk rows per chunk-attention work item
 constexpr int PARTS_ROWS = 512;   // split-K partials are sized for batches up to this many rows (larger
                                   // batches fill the GPU without splitting; with less room fewer splits run)
 
@@ -108,7 +108,7 @@ Layout make_layout(const sarathi_model_cfg* c, int T, int n_chunks, int S) {
   const size_t max_pre = ((size_t)(T + QBLOCK - 1) / QBLOCK + n_chunks - 1) * ((S + PRE_SPLIT - 1) / PRE_SPLIT);
   const size_t max_dec = (size_t)T * ((S + SPLIT_KEYS - 1) / SPLIT_KEYS);
   L.part = take((max_pre * QBLOCK + max_dec) * c->n_heads * (c->head_dim + 2) * 4);
-  L.meta = take(((size_t)T * 5 + (size_t)n_chunks * 4 + max_pre * 2 + max_dec) * 4);
+  L.meta = take(((size_t)T * 5 + (size_t)n_chunks * 4 + max_pre * 3 + max_dec) * 4);
   L.ping0 = take(T * H * es);
   L.ping1 = take(T * H * es);
   L.total = off;
@@ -163,9 +163,9 @@ int from_mixed(const sarathi_mixed_batch* b, BatchDesc* out) {
 
 // Host-side description of the batch and its device metadata.
 struct Plan {
-  int C, B, T, row_base, n_pre, n_dec, n_chunks;
+  int C, B, T, row_base, n_pre, n_dec, n_chunks, pre_split;
   // row_slot[T] row_pos[T] comb[3T] chunk table [n_chunks][slot, offset, len, first row]
-  // pre_work[n_pre][chunk, (q_block << 12) | key_split] dec_work[n_dec]
+  // pre_work[n_pre][chunk, (q_block << 12) | key_split, partial slot] dec_work[n_dec]
   std::vector<int> meta;
   size_t o_slot, o_pos, o_comb, o_chunks, o_pre, o_dec;   // int offsets into meta
 };
@@ -213,6 +213,7 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
   // item = row x key split).  fp32: every row goes to row attention (a chunk
   // row at position p is attention over keys 0..p, like a decode with ctx = p).
   p.row_base = (cfg->dtype == SARATHI_BF16) ? p.C : 0;
+  p.pre_split = PRE_SPLIT;
   std::vector<int> slot(p.T), pos(p.T), comb(3 * p.T), tab, pre, dec;
   int r0 = 0;
   for (const ChunkDesc& c : b.chunks) {
@@ -222,24 +223,49 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
   }
   for (int i = 0; i < p.B; ++i) { slot[p.C + i] = b.dslots[i]; pos[p.C + i] = b.dctx[i]; }
   if (p.row_base > 0) {
+    // Partial slots run q-block by q-block (a row's splits are consecutive,
+    // QBLOCK partial rows apart); the work items run split by split so that
+    // the query blocks that read the same keys are neighbours (and share an
+    // XCD's L2, see the chunk-attention kernel).
+    // Key split: the largest (PRE_SPLIT x 2^j) that still gives every CU a
+    // block (fewer, longer items write fewer partials); PRE_SPLIT when even
+    // that leaves CUs idle.
+    auto n_blocks = [&](int split) {
+      long n = 0;
+      for (const ChunkDesc& c : b.chunks)
+        for (int qb = 0; qb * QBLOCK < c.len; ++qb)
+          n += (c.offset + std::min((qb + 1) * QBLOCK, c.len) + split - 1) / split;
+      return n * cfg->n_heads;
+    };
+    p.pre_split = PRE_SPLIT;
+    while (p.pre_split < (1 << 20) && n_blocks(2 * p.pre_split) >= 256) p.pre_split *= 2;
+    const int split = p.pre_split;
     r0 = 0;
+    int slot_base = 0;
     for (int ci = 0; ci < p.n_chunks; ++ci) {
       const ChunkDesc& c = b.chunks[ci];
-      for (int qb = 0; qb * QBLOCK < c.len; ++qb) {
+      const int nqb = (c.len + QBLOCK - 1) / QBLOCK;
+      std::vector<int> ns(nqb), first(nqb);
+      int max_ns = 0;
+      for (int qb = 0; qb < nqb; ++qb) {
         const int n_keys = c.offset + std::min((qb + 1) * QBLOCK, c.len);
-        const int ns = (n_keys + PRE_SPLIT - 1) / PRE_SPLIT;
-        const int first = (int)pre.size() / 2;
-        for (int s = 0; s < ns; ++s) pre.insert(pre.end(), {ci, (qb << 12) | s});
+        ns[qb] = (n_keys + split - 1) / split;
+        first[qb] = slot_base;
+        slot_base += ns[qb];
+        max_ns = std::max(max_ns, ns[qb]);
         for (int r = qb * QBLOCK; r < std::min((qb + 1) * QBLOCK, c.len); ++r) {
-          comb[3 * (r0 + r)] = first * QBLOCK + (r - qb * QBLOCK);
-          comb[3 * (r0 + r) + 1] = ns;
+          comb[3 * (r0 + r)] = first[qb] * QBLOCK + (r - qb * QBLOCK);
+          comb[3 * (r0 + r) + 1] = ns[qb];
           comb[3 * (r0 + r) + 2] = QBLOCK;
         }
       }
+      for (int s = 0; s < max_ns; ++s)
+        for (int qb = 0; qb < nqb; ++qb)
+          if (s < ns[qb]) pre.insert(pre.end(), {ci, (qb << 12) | s, first[qb] + s});
       r0 += c.len;
     }
   }
-  const int pre_rows = (int)pre.size() / 2 * QBLOCK;
+  const int pre_rows = (int)pre.size() / 3 * QBLOCK;
   for (int r = p.row_base; r < p.T; ++r) {
     const int ns = (pos[r] + 1 + SPLIT_KEYS - 1) / SPLIT_KEYS;
     comb[3 * r] = pre_rows + (int)dec.size();
@@ -247,7 +273,7 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
     comb[3 * r + 2] = 1;
     for (int s = 0; s < ns; ++s) dec.push_back(((r - p.row_base) << 12) | s);
   }
-  p.n_pre = (int)pre.size() / 2;
+  p.n_pre = (int)pre.size() / 3;
   p.n_dec = (int)dec.size();
   p.meta.reserve(5 * p.T + tab.size() + pre.size() + dec.size());
   p.o_slot = 0; p.meta.insert(p.meta.end(), slot.begin(), slot.end());
@@ -365,7 +391,7 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
     PrefillArgs pa{};
     pa.qkv = ws + c.L.qkv; pa.ld_qkv = 3 * QD; pa.kv_layer = kv_layer; pa.st = c.kv->st;
     pa.chunks = meta + P.o_chunks; pa.nh = nh; pa.hd = hd;
-    pa.work = meta + P.o_pre; pa.n_work = P.n_pre; pa.split_keys = PRE_SPLIT; pa.part = part;
+    pa.work = meta + P.o_pre; pa.n_work = P.n_pre; pa.split_keys = P.pre_split; pa.part = part;
     e = launch_attn_prefill(dt, pa, c.s);
     if (e != hipSuccess) return hip_fail(e, "chunk attention");
   }
