@@ -27,6 +27,7 @@ struct GemmP {
   int M, N, K;          // N = output columns (SwiGLU: F)
   int k_split, n_split; // K elements per split; number of splits
   int tiles_m, tiles_n, n_tiles;
+  int rotate_k;         // gemm_ws_kernel: the M-tiles of a W panel stream its k-tiles in rotated orders
   void* out;            // [M, N]: dtype, or fp32 for EPI_RESID_TO_F32; EPI_PARTIAL: fp32 [n_split][M, N]
   const void* resid;    // EPI_RESID_TO_F32: dtype [M,N]; EPI_RESIDF32_TO_ACT: fp32 [M,N]
 };
@@ -286,7 +287,17 @@ __global__ __launch_bounds__(64 * (WGM * WGN + NP)) void gemm_ws_kernel(GemmP p)
                       : W + (size_t)w_row_of<EPI, WTN>(row - BM, n0_out, p.N) * p.K + kbeg + lchunk * 8;
     }
     const bool extra = q < RHI;
+    // With rotate_k, the G = tiles_m blocks that share a W panel take each
+    // group of G k-tiles in rotated orders (block m starts at m), so every
+    // k-tile of the panel is first requested by one block -- which pays the
+    // HBM latency -- and found in L2 by the others a step later, instead of
+    // all G waiting on the same miss.
+    const int G = p.rotate_k ? p.tiles_m : 1;
     auto issue = [&](int stage, int kt) {
+      if (G > 1) {
+        const int base = kt / G * G;
+        if (base + G <= nk) kt = base + (kt - base + tile_m) % G;
+      }
       uint4* dst = lds + stage * ROWS * 8;
 #pragma unroll
       for (int j = IHI - 1; j >= 0; --j)
@@ -628,6 +639,9 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s) {
   const int out_per_tile = swiglu ? BN / 2 : BN;
   p.tiles_m = (a.M + BM - 1) / BM;
   p.tiles_n = (a.N + out_per_tile - 1) / out_per_tile;
+  // rotated k order pays off for two M-tiles over 128-row W panels (measured:
+  // -13% on preproj at 320 rows; no gain with 256-row panels or four M-tiles)
+  p.rotate_k = (ws && BN == 128 && p.tiles_m == 2) ? 1 : 0;
 
   // Split-K for the residual ops when the tile grid leaves CUs idle: every
   // split stores its fp32 partial, then one pass adds residual + partials in
