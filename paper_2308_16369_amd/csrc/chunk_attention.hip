@@ -1,6 +1,6 @@
-// Attention of the hybrid batch, run separately for the prefill chunk and for
-// the decodes (Sec. 4.3).  Both write per-split partial results
-// (max, sum, unnormalised o) that one combine pass merges per row.
+// Attention of the prompt chunk(s) of the hybrid batch, run separately from the
+// decodes (Sec. 4.3).  It writes per-split partial results (max, sum,
+// unnormalised o) that the combine pass of decode_attention.hip merges per row.
 //
 // Chunked-prefill attention (bf16, MFMA): the chunk's queries at positions
 // off..off+C-1 attend to the prefill slot's keys 0..position (the earlier
@@ -10,14 +10,6 @@
 // keys are staged in a ring of LDS stages by LDS DMA (V read back transposed
 // so P*V takes 16 contiguous bytes per lane); S = Q K^T and O += P V run on
 // v_mfma_f32_16x16x32_bf16 with an fp32 online softmax.
-//
-// Row attention (decodes; in fp32 runs also the chunk rows): each row attends
-// to keys 0..pos of its slot.  Work item = (row, split of split_keys keys); a
-// block of 4 waves streams its split, each wave 32 keys per pass with 16-byte
-// loads (a key row spread over hd*size/16 lanes), partial dot products
-// reduce-scattered across those lanes so each key's score ends up in two
-// lanes, wave-level online softmax, then P*V accumulated per lane.  The
-// block's four wave states are merged in LDS into one partial.
 #include "kernels.h"
 
 namespace sarathi {
@@ -262,217 +254,6 @@ hipError_t launch_attn_prefill(int dtype, const PrefillArgs& a, hipStream_t s) {
   // two stages (64 KB for head_dim 128): two blocks per CU
   if (a.hd == 128) return run_prefill<128, NW, 2>(a, grid, scale_log2, s);
   return run_prefill<64, NW, 2>(a, grid, scale_log2, s);
-}
-
-// ============================================================================ row attention
-template <typename T, int D, int DUP>
-__global__ __launch_bounds__(256) void attn_rows_kernel(RowAttnArgs a, float scale_log2) {
-  constexpr int EPL = Vec16<T>::N;           // elements per lane per key (16 bytes)
-  constexpr int LPK = D / EPL;               // lanes per key row
-  constexpr int KPI = 64 / LPK;              // keys per wave load instruction
-  constexpr int NI = LPK / DUP;              // load instructions per pass
-  constexpr int KP = NI * KPI;               // keys per pass per wave (64 / DUP)
-  static_assert(LPK * KPI == 64 && NI * DUP == LPK, "pass");
-  __shared__ float red_m[4], red_l[4];
-  __shared__ float red_o[4][D];
-
-  const int item = blockIdx.x, h = blockIdx.y;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int g = lane / LPK, j = lane % LPK;
-  const int wv = a.work[item];
-  const int row_rel = wv >> 12, split = wv & 4095;
-  const int row = a.row_base + row_rel;
-  const int slot = a.row_slot[row];
-  const int nk = a.row_pos[row] + 1;
-  const int kb = split * a.split_keys;
-  const int ke = min(nk, kb + a.split_keys);
-
-  const T* qkv = reinterpret_cast<const T*>(a.qkv);
-  const T* cache = reinterpret_cast<const T*>(a.kv_layer);
-  const T* kbase = cache + (size_t)slot * a.st.slot + (size_t)h * a.st.head + j * EPL;
-  const T* vbase = kbase + a.st.kv;
-
-  float q[EPL];
-  Vec16<T>::unpack(*reinterpret_cast<const uint4*>(qkv + (size_t)row * a.ld_qkv + h * D + j * EPL), q);
-#pragma unroll
-  for (int e = 0; e < EPL; ++e) q[e] *= scale_log2;
-
-  float m_run = -INFINITY, l_run = 0.f;
-  float o[EPL];
-#pragma unroll
-  for (int e = 0; e < EPL; ++e) o[e] = 0.f;
-
-  // Each wave takes passes of KP keys (pb, pb + 4*KP, ...).  All K loads are
-  // issued first, then all V loads: the scores wait only for K (loads
-  // complete in order) while V is still in flight.  Key addresses past the
-  // split are clamped to its last key (finite data, masked below).
-  for (int pb = kb + wave * KP; pb < ke; pb += 4 * KP) {
-    uint4 kr[NI], vr[NI];
-#pragma unroll
-    for (int i = 0; i < NI; ++i)
-      kr[i] = *reinterpret_cast<const uint4*>(kbase + (size_t)min(pb + i * KPI + g, ke - 1) * a.st.pos);
-#pragma unroll
-    for (int i = 0; i < NI; ++i)
-      vr[i] = *reinterpret_cast<const uint4*>(vbase + (size_t)min(pb + i * KPI + g, ke - 1) * a.st.pos);
-    // Keep all 2*NI loads in flight before any use (the scheduler would
-    // otherwise sink each load next to its first use and serialise them).
-    __builtin_amdgcn_sched_barrier(0);
-    float part[NI];
-#pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      float kf[EPL];
-      Vec16<T>::unpack(kr[i], kf);
-      float acc = 0.f;
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) acc = fmaf(q[e], kf[e], acc);
-      part[i] = acc;
-    }
-    // Reduce-scatter across the LPK lanes of a key group: afterwards the
-    // DUP lanes j with j / DUP == i hold the full score of the key loaded
-    // by instruction i.
-#pragma unroll
-    for (int n = NI, msk = LPK / 2; n > 1; n >>= 1, msk >>= 1) {
-#pragma unroll
-      for (int idx = 0; idx < n / 2; ++idx) {
-        const bool upper = (j & msk) != 0;
-        const float keep = upper ? part[idx + n / 2] : part[idx];
-        const float send = upper ? part[idx] : part[idx + n / 2];
-        part[idx] = keep + __shfl_xor(send, msk, 64);
-      }
-    }
-#pragma unroll
-    for (int msk = DUP / 2; msk >= 1; msk >>= 1) part[0] += __shfl_xor(part[0], msk, 64);
-    const int mykey = pb + (j / DUP) * KPI + g;
-    const bool own = (j % DUP) == 0;            // one lane per key counts in the sum
-    const float sc = (mykey < ke) ? part[0] : -INFINITY;
-    const float m_new = fmaxf(m_run, wave_max(sc));
-    const float m_safe = (m_new == -INFINITY) ? 0.f : m_new;
-    const float corr = exp2f(m_run - m_safe);
-    const float pk = (mykey < ke) ? exp2f(sc - m_safe) : 0.f;
-    l_run = l_run * corr + wave_sum(own ? pk : 0.f);
-    m_run = m_new;
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) o[e] *= corr;
-#pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const float w = __shfl(pk, g * LPK + i * DUP, 64);
-      float vf[EPL];
-      Vec16<T>::unpack(vr[i], vf);
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) o[e] = fmaf(w, vf[e], o[e]);
-    }
-  }
-  // Sum o over the KPI key groups of the wave.
-#pragma unroll
-  for (int msk = LPK; msk < 64; msk <<= 1)
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) o[e] += __shfl_xor(o[e], msk, 64);
-
-  if (lane == 0) {
-    red_m[wave] = m_run;
-    red_l[wave] = l_run;
-  }
-  if (g == 0) {
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) red_o[wave][j * EPL + e] = o[e];
-  }
-  __syncthreads();
-  float M = fmaxf(fmaxf(red_m[0], red_m[1]), fmaxf(red_m[2], red_m[3]));
-  const float Ms = (M == -INFINITY) ? 0.f : M;
-  float* dst = a.part + ((size_t)(a.part_base + item) * a.nh + h) * (D + 2);
-  for (int d = tid; d < D; d += 256) {
-    float acc = 0.f;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) acc += red_o[w][d] * exp2f(red_m[w] - Ms);
-    dst[2 + d] = acc;
-  }
-  if (tid == 0) {
-    float L = 0.f;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) L += red_l[w] * exp2f(red_m[w] - Ms);
-    dst[0] = M;
-    dst[1] = L;
-  }
-}
-
-template <typename T, int D>
-static hipError_t run_rows(const RowAttnArgs& a, hipStream_t s) {
-  const float scale_log2 = LOG2E / sqrtf((float)D);
-  hipLaunchKernelGGL((attn_rows_kernel<T, D, 2>), dim3(a.n_work, a.nh), dim3(256), 0, s, a, scale_log2);
-  return hipGetLastError();
-}
-
-hipError_t launch_attn_rows(int dtype, const RowAttnArgs& a, hipStream_t s) {
-  if (a.n_work <= 0) return hipSuccess;
-  if (dtype == 0) return a.hd == 128 ? run_rows<float, 128>(a, s) : run_rows<float, 64>(a, s);
-  return a.hd == 128 ? run_rows<bf16, 128>(a, s) : run_rows<bf16, 64>(a, s);
-}
-
-// ============================================================================ combine
-// O = sum_s o_s 2^(m_s - M) / sum_s l_s 2^(m_s - M), M = max_s m_s.  One wave
-// per (row, head), four heads per block: the lanes read the splits' (m, l)
-// pairs in parallel, then every lane accumulates its D/64 columns over the
-// splits with independent loads.
-template <typename T, int D>
-__global__ __launch_bounds__(256) void attn_combine_kernel(CombineArgs a) {
-  constexpr int E = D / 64;
-  const int r = blockIdx.x, lane = threadIdx.x & 63;
-  const int h = blockIdx.y * 4 + (threadIdx.x >> 6);
-  if (h >= a.nh) return;
-  const int start = a.comb[3 * r], cnt = a.comb[3 * r + 1], stride = a.comb[3 * r + 2];
-  auto src_of = [&](int j) { return a.part + ((size_t)(start + j * stride) * a.nh + h) * (D + 2); };
-  float M = -INFINITY;
-  for (int j0 = 0; j0 < cnt; j0 += 64)
-    if (j0 + lane < cnt) M = fmaxf(M, src_of(j0 + lane)[0]);
-  M = wave_max(M);
-  const float Ms = (M == -INFINITY) ? 0.f : M;
-  float L = 0.f;
-  float acc[E];
-#pragma unroll
-  for (int e = 0; e < E; ++e) acc[e] = 0.f;
-  for (int j0 = 0; j0 < cnt; j0 += 64) {
-    const int nj = min(64, cnt - j0);
-    const float* mine = src_of(j0 + min(lane, nj - 1));
-    const float wl = lane < nj ? exp2f(mine[0] - Ms) : 0.f;
-    L += wl * (lane < nj ? mine[1] : 0.f);
-    int j = 0;
-    for (; j + 4 <= nj; j += 4) {
-      float v[4][E];
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int e = 0; e < E; ++e) v[u][e] = src_of(j0 + j + u)[2 + lane + 64 * e];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const float w = __shfl(wl, j + u, 64);
-#pragma unroll
-        for (int e = 0; e < E; ++e) acc[e] = fmaf(v[u][e], w, acc[e]);
-      }
-    }
-    for (; j < nj; ++j) {
-      const float w = __shfl(wl, j, 64);
-#pragma unroll
-      for (int e = 0; e < E; ++e) acc[e] = fmaf(src_of(j0 + j)[2 + lane + 64 * e], w, acc[e]);
-    }
-  }
-  L = wave_sum(L);
-  const float inv = 1.0f / L;
-  T* out = reinterpret_cast<T*>(a.out) + (size_t)r * a.ld_out + h * D;
-#pragma unroll
-  for (int e = 0; e < E; ++e) out[lane + 64 * e] = from_f<T>(acc[e] * inv);
-}
-
-hipError_t launch_attn_combine(int dtype, const CombineArgs& a, hipStream_t s) {
-  if (a.n_rows <= 0) return hipSuccess;
-  dim3 grid(a.n_rows, (a.nh + 3) / 4);
-  if (dtype == 0) {
-    if (a.hd == 128) hipLaunchKernelGGL((attn_combine_kernel<float, 128>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((attn_combine_kernel<float, 64>), grid, dim3(256), 0, s, a);
-  } else {
-    if (a.hd == 128) hipLaunchKernelGGL((attn_combine_kernel<bf16, 128>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((attn_combine_kernel<bf16, 64>), grid, dim3(256), 0, s, a);
-  }
-  return hipGetLastError();
 }
 
 }  // namespace sarathi

@@ -27,7 +27,8 @@ struct GemmP {
   int M, N, K;          // N = output columns (SwiGLU: F)
   int k_split, n_split; // K elements per split; number of splits
   int tiles_m, tiles_n, n_tiles;
-  int rotate_k;         // gemm_ws_kernel: the M-tiles of a W panel stream its k-tiles in rotated orders
+  int rotate_k;         // gemm_ws_kernel: 0, or the distance (in k-tiles) by which the M-tiles of a W panel
+                        // rotate their k-tile order
   void* out;            // [M, N]: dtype, or fp32 for EPI_RESID_TO_F32; EPI_PARTIAL: fp32 [n_split][M, N]
   const void* resid;    // EPI_RESID_TO_F32: dtype [M,N]; EPI_RESIDF32_TO_ACT: fp32 [M,N]
 };
@@ -292,11 +293,11 @@ __global__ __launch_bounds__(64 * (WGM * WGN + NP)) void gemm_ws_kernel(GemmP p)
     // k-tile of the panel is first requested by one block -- which pays the
     // HBM latency -- and found in L2 by the others a step later, instead of
     // all G waiting on the same miss.
-    const int G = p.rotate_k ? p.tiles_m : 1;
+    const int G = p.rotate_k ? p.tiles_m : 1, RD = p.rotate_k, GR = G * RD;
     auto issue = [&](int stage, int kt) {
       if (G > 1) {
-        const int base = kt / G * G;
-        if (base + G <= nk) kt = base + (kt - base + tile_m) % G;
+        const int base = kt / GR * GR;
+        if (base + GR <= nk) kt = base + (kt - base + tile_m * RD) % GR;
       }
       uint4* dst = lds + stage * ROWS * 8;
 #pragma unroll
