@@ -16,6 +16,8 @@
 // with the same epilogues.
 #include "kernels.h"
 
+#include <algorithm>
+
 namespace sarathi {
 
 enum Epi { EPI_STORE = 0, EPI_GELU = 1, EPI_SWIGLU = 2, EPI_RESID_TO_F32 = 3, EPI_RESIDF32_TO_ACT = 4,
@@ -541,19 +543,28 @@ static int pick_cfg(int M, int n_panels) {
   return CFG_64x128;
 }
 
-// Producer/consumer tiles (BM x BN W rows; consumer waves 2 x 4, or 2 x 2
-// for BN = 64; 4 producer waves) and their LDS ring depth (~100-156 KB).
-enum WsCfg { WS_64x64 = 0, WS_64x128, WS_64x256, WS_96x128, WS_96x256, WS_160x128, WS_160x256 };
+// Producer/consumer tiles (BM x BN W rows; consumer waves 2 x (BN / 32), or
+// 2 x 2 for BN = 64; 4 producer waves, 2 beside 14 consumers) and their LDS
+// ring depth (~100-156 KB).
+struct WsTile {
+  int bm, bn;
+};
+constexpr WsTile kWsTiles[] = {{64, 64},   {64, 128},  {64, 256},  {96, 128},  {96, 192},
+                               {96, 256},  {160, 128}, {160, 192}, {160, 224}, {160, 256}};
+constexpr int kNumWsTiles = sizeof(kWsTiles) / sizeof(kWsTiles[0]);
 
 template <int EPI>
 static hipError_t run_ws_cfg(int cfg, const GemmP& p, hipStream_t s) {
   switch (cfg) {
-    case WS_64x64: return run_ws<64, 64, 2, 2, 4, 6, EPI>(p, s);
-    case WS_64x128: return run_ws<64, 128, 2, 4, 4, 6, EPI>(p, s);
-    case WS_64x256: return run_ws<64, 256, 2, 4, 4, 3, EPI>(p, s);
-    case WS_96x128: return run_ws<96, 128, 2, 4, 4, 5, EPI>(p, s);
-    case WS_96x256: return run_ws<96, 256, 2, 4, 4, 3, EPI>(p, s);
-    case WS_160x128: return run_ws<160, 128, 2, 4, 4, 4, EPI>(p, s);
+    case 0: return run_ws<64, 64, 2, 2, 4, 6, EPI>(p, s);
+    case 1: return run_ws<64, 128, 2, 4, 4, 6, EPI>(p, s);
+    case 2: return run_ws<64, 256, 2, 4, 4, 3, EPI>(p, s);
+    case 3: return run_ws<96, 128, 2, 4, 4, 5, EPI>(p, s);
+    case 4: return run_ws<96, 192, 2, 6, 4, 4, EPI>(p, s);
+    case 5: return run_ws<96, 256, 2, 4, 4, 3, EPI>(p, s);
+    case 6: return run_ws<160, 128, 2, 4, 4, 4, EPI>(p, s);
+    case 7: return run_ws<160, 192, 2, 6, 4, 3, EPI>(p, s);
+    case 8: return run_ws<160, 224, 2, 7, 2, 3, EPI>(p, s);
     default: return run_ws<160, 256, 2, 4, 4, 3, EPI>(p, s);
   }
 }
@@ -569,31 +580,42 @@ static hipError_t run_ws_epi(int epi, int cfg, const GemmP& p, hipStream_t s) {
   }
 }
 
-static int ws_bm(int cfg) { return cfg <= WS_64x256 ? 64 : (cfg <= WS_96x256 ? 96 : 160); }
-static int ws_bn(int cfg) {
-  return cfg == WS_64x64 ? 64 : ((cfg == WS_64x256 || cfg == WS_96x256 || cfg == WS_160x256) ? 256 : 128);
-}
-
-// A CU's operand feed is bounded by its outstanding memory requests, so the
-// tile shape sets the speed: the tallest block that pads M little (fewer W
-// re-reads), then the widest block (fewer A re-reads) that still leaves
-// >= 200 blocks for the 256 CUs.  The split-K ops fill the GPU through their
-// splits: 256 W rows for 160-row blocks, 128 for shorter ones.
-static int pick_ws(int M, int n_out, bool swiglu, bool split_ok) {
-  const int bm = M <= 64 ? 64 : (M <= 96 ? 96 : 160);
-  const int tiles_m = (M + bm - 1) / bm;
-  auto tiles = [&](int bn) {
+// Tile (and K-split) choice from a cost model of the operand feed, fitted to
+// MI355X measurements of the LLaMA-13B / 33B shapes.  Each CU runs one block
+// at a time and is bound by its outstanding memory requests: a 64-wide k-tile
+// costs ~1.9 ns per A row (L2 hits) and ~3.1 ns per W row when two M-tiles
+// share the W panel (~4.2 ns when one block streams it alone: every row an
+// HBM miss); a block adds ~3 us of pipeline fill plus its output writes
+// (~40 GB/s per CU); blocks beyond the first 256 run as another round.  A
+// split-K op's reduction pass reads the fp32 partials and writes the result
+// at ~5.5 TB/s.
+struct WsChoice {
+  int cfg, n_split;
+};
+static WsChoice pick_ws(int M, int N, int K, bool swiglu, int max_split) {
+  WsChoice best{6, 1};
+  double best_t = 1e300;
+  const int nk = K / 64;
+  for (int c = 0; c < kNumWsTiles; ++c) {
+    const int bm = kWsTiles[c].bm, bn = kWsTiles[c].bn;
+    if (bm == 64 && M > 64) continue;    // 64-row tiles only for short batches
     const int per = swiglu ? bn / 2 : bn;
-    return tiles_m * ((n_out + per - 1) / per);
-  };
-  int bn;
-  if (split_ok) bn = bm == 160 ? 256 : 128;
-  else if (tiles(256) >= 200) bn = 256;
-  else if (tiles(128) >= 200 || bm != 64) bn = 128;
-  else bn = 64;
-  if (bm == 64) return bn == 64 ? WS_64x64 : (bn == 128 ? WS_64x128 : WS_64x256);
-  if (bm == 96) return bn == 256 ? WS_96x256 : WS_96x128;
-  return bn == 256 ? WS_160x256 : WS_160x128;
+    const int tiles_m = (M + bm - 1) / bm;
+    const long tiles = (long)tiles_m * ((N + per - 1) / per);
+    const double per_k = 1.9e-3 * bm + (tiles_m >= 2 ? 3.1e-3 : 4.2e-3) * bn;   // us per k-tile
+    for (int ns = 1; ns <= max_split; ++ns) {
+      const double rounds = (double)((tiles * ns + 255) / 256);
+      const double k_tiles = 2.0 * ((nk / 2 + ns - 1) / ns);               // whole pairs per split
+      const double out_bytes = (double)bm * (swiglu ? bn / 2 : bn) * (ns > 1 ? 4.0 : 2.0);
+      double t = rounds * (k_tiles * per_k + 3.0 + out_bytes / 4.0e4);
+      if (ns > 1) t += (ns * 4.0 + 6.0) * (double)M * N / 5.5e6 + 2.0;
+      if (t < best_t * 0.999) {
+        best_t = t;
+        best = {c, ns};
+      }
+    }
+  }
+  return best;
 }
 
 hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s) {
@@ -625,11 +647,21 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s) {
   const bool resid_kind = a.kind == LIN_RESID || a.kind == LIN_RESID_F32IN;
   const bool ws = (a.K % 64) == 0;   // producer/consumer kernel: whole 64-wide k-tiles
 
-  int cfg, BM, BN;
+  // splits available to the residual ops: whole groups of two k-tiles per
+  // split, partials must fit the scratch
+  int max_split = 1;
+  if (resid_kind && a.parts != nullptr) {
+    max_split = std::min(MAX_SPLIT, (a.K + 127) / 128 / 2);
+    max_split = (int)std::min<size_t>((size_t)max_split, a.parts_cap / ((size_t)a.M * a.N));
+    max_split = std::max(max_split, 1);
+  }
+  int cfg, BM, BN, ws_split = 1;
   if (ws) {
-    cfg = pick_ws(a.M, a.N, swiglu, resid_kind && a.parts != nullptr);
-    BM = ws_bm(cfg);
-    BN = ws_bn(cfg);
+    const WsChoice ch = pick_ws(a.M, a.N, a.K, swiglu, max_split);
+    cfg = ch.cfg;
+    ws_split = ch.n_split;
+    BM = kWsTiles[cfg].bm;
+    BN = kWsTiles[cfg].bn;
   } else {
     BN = 128;
     const int n_panels = (a.N + (swiglu ? BN / 2 : BN) - 1) / (swiglu ? BN / 2 : BN);
@@ -651,9 +683,9 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s) {
   // count keeps the grid within one wave of blocks over the 256 CUs.
   const int tiles = p.tiles_m * p.tiles_n;
   int n_split = 1;
-  if (resid_kind && a.parts != nullptr && tiles < 256) {
+  if (resid_kind && a.parts != nullptr && (ws ? ws_split > 1 : tiles < 256)) {
     const int kgroups = (a.K + 127) / 128;
-    int ns = (ws || cfg == CFG_320x128) ? 256 / tiles : (400 + tiles - 1) / tiles;
+    int ns = ws ? ws_split : (cfg == CFG_320x128 ? 256 / tiles : (400 + tiles - 1) / tiles);
     if (ns > kgroups / 2) ns = kgroups / 2;
     if (ns > MAX_SPLIT) ns = MAX_SPLIT;
     if ((size_t)ns * a.M * a.N > a.parts_cap) ns = (int)(a.parts_cap / ((size_t)a.M * a.N));

@@ -11,7 +11,11 @@ namespace sarathi {
 
 // ---- batch metadata (int32 arrays in the workspace), written by a kernel
 // whose arguments carry the host values (stream-ordered, no staging buffer).
-constexpr int META_CHUNK = 640;
+// 8 KB of kernel arguments per launch: one launch covers the metadata of a
+// batch of ~350 rows (5 ints per row plus the work lists); ROCm passes
+// argument structs of this size (measured: one 8 KB launch costs about as much
+// as one small launch, against three for 2.5 KB pieces).
+constexpr int META_CHUNK = 2040;
 struct MetaChunk {
   int count;
   int values[META_CHUNK];
