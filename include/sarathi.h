@@ -288,6 +288,23 @@ int sarathi_linear(int dtype, int kind, int M, int N, int K, const void* x, cons
                    const void* resid, void* out, void* scratch, size_t scratch_bytes,
                    void* hip_stream);
 
+/*
+ * Tile shapes of the bf16 matmul kernel, for tests and tuning:
+ * sarathi_linear_tile_count() shapes, shape t = *bm rows of x by *bn rows of
+ * W per block (sarathi_linear_tile_shape returns EINVAL for t out of range).
+ * sarathi_linear_tiled is sarathi_linear with the shape and K-split count
+ * given instead of chosen by the library's cost model: dtype must be BF16 and
+ * K a multiple of 64 (else EUNSUPPORTED); n_split >= 1 is used for the two
+ * residual kinds when `scratch` holds n_split x M x N fp32 (capped at 6 and
+ * at one split per 128 of K), and ignored for the other kinds.  Results
+ * differ from sarathi_linear only in the fp32 summation order.
+ */
+int sarathi_linear_tile_count(void);
+int sarathi_linear_tile_shape(int tile, int* bm, int* bn);
+int sarathi_linear_tiled(int kind, int M, int N, int K, const void* x, const void* w, const void* resid,
+                         void* out, void* scratch, size_t scratch_bytes, int tile, int n_split,
+                         void* hip_stream);
+
 /* ------------------------------------------------------------------ stage timing */
 /*
  * Measurement hook: between sarathi_profile_begin and sarathi_profile_end,

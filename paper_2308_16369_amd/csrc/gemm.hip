@@ -618,7 +618,15 @@ static WsChoice pick_ws(int M, int N, int K, bool swiglu, int max_split) {
   return best;
 }
 
-hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s) {
+int linear_tile_count() { return kNumWsTiles; }
+bool linear_tile_shape(int tile, int* bm, int* bn) {
+  if (tile < 0 || tile >= kNumWsTiles) return false;
+  *bm = kWsTiles[tile].bm;
+  *bn = kWsTiles[tile].bn;
+  return true;
+}
+
+hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s, int force_tile, int force_split) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
   GemmP p{};
   p.A = a.x; p.W = a.w; p.M = a.M; p.N = a.N; p.K = a.K;
@@ -657,7 +665,8 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s) {
   }
   int cfg, BM, BN, ws_split = 1;
   if (ws) {
-    const WsChoice ch = pick_ws(a.M, a.N, a.K, swiglu, max_split);
+    WsChoice ch = pick_ws(a.M, a.N, a.K, swiglu, max_split);
+    if (force_tile >= 0 && force_tile < kNumWsTiles) ch = {force_tile, std::min(std::max(force_split, 1), max_split)};
     cfg = ch.cfg;
     ws_split = ch.n_split;
     BM = kWsTiles[cfg].bm;

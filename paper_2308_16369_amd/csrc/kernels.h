@@ -52,7 +52,12 @@ struct LinearArgs {
   size_t parts_cap;     // its capacity in floats
 };
 constexpr int MAX_SPLIT = 6;   // split-K partials: at most MAX_SPLIT x [M, N] fp32
-hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s);
+// force_tile >= 0 (bf16, K a multiple of 64): run that producer/consumer tile
+// shape with force_split K-splits (residual kinds with scratch) instead of the
+// cost model's choice.
+hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s, int force_tile = -1, int force_split = 0);
+int linear_tile_count();
+bool linear_tile_shape(int tile, int* bm, int* bn);
 
 // ---- attention
 // Partial results (one per row x head x key split): [m, l, o[hd]] in fp32,

@@ -266,7 +266,13 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
     }
   }
   const int pre_rows = (int)pre.size() / 3 * QBLOCK;
-  for (int r = p.row_base; r < p.T; ++r) {
+  // Row-attention items run in the order of the rows' KV slots (each row's
+  // splits together), so the blocks in flight stream the cache in address
+  // order (measured ~2% faster than a random slot order).
+  std::vector<int> order;
+  for (int r = p.row_base; r < p.T; ++r) order.push_back(r);
+  std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return slot[x] < slot[y]; });
+  for (int r : order) {
     const int ns = (pos[r] + 1 + SPLIT_KEYS - 1) / SPLIT_KEYS;
     comb[3 * r] = pre_rows + (int)dec.size();
     comb[3 * r + 1] = ns;
@@ -677,8 +683,9 @@ size_t sarathi_linear_scratch_bytes(int M, int N) {
   return (size_t)MAX_SPLIT * M * N * 4;
 }
 
-int sarathi_linear(int dtype, int kind, int M, int N, int K, const void* x, const void* w, const void* resid,
-                   void* out, void* scratch, size_t scratch_bytes, void* hip_stream) {
+namespace {
+int linear_common(int dtype, int kind, int M, int N, int K, const void* x, const void* w, const void* resid,
+                  void* out, void* scratch, size_t scratch_bytes, void* hip_stream, int tile, int n_split) {
   if (dtype != SARATHI_F32 && dtype != SARATHI_BF16) return fail(SARATHI_EUNSUPPORTED, "dtype %d", dtype);
   if (kind < SARATHI_LINEAR_PLAIN || kind > SARATHI_LINEAR_GELU) return fail(SARATHI_EINVAL, "kind %d", kind);
   if (M < 1 || N < 1 || K < 1) return fail(SARATHI_EINVAL, "M, N, K must be positive");
@@ -693,9 +700,32 @@ int sarathi_linear(int dtype, int kind, int M, int N, int K, const void* x, cons
     a.parts = static_cast<float*>(scratch);
     a.parts_cap = scratch_bytes / 4;
   }
-  hipError_t e = launch_linear(dtype, a, static_cast<hipStream_t>(hip_stream));
+  hipError_t e = launch_linear(dtype, a, static_cast<hipStream_t>(hip_stream), tile, n_split);
   if (e != hipSuccess) return hip_fail(e, "linear");
   return SARATHI_OK;
+}
+}  // namespace
+
+int sarathi_linear(int dtype, int kind, int M, int N, int K, const void* x, const void* w, const void* resid,
+                   void* out, void* scratch, size_t scratch_bytes, void* hip_stream) {
+  return linear_common(dtype, kind, M, N, K, x, w, resid, out, scratch, scratch_bytes, hip_stream, -1, 0);
+}
+
+int sarathi_linear_tile_count(void) { return linear_tile_count(); }
+
+int sarathi_linear_tile_shape(int tile, int* bm, int* bn) {
+  if (!bm || !bn) return fail(SARATHI_EINVAL, "NULL pointer");
+  if (!linear_tile_shape(tile, bm, bn)) return fail(SARATHI_EINVAL, "tile %d outside [0, %d)", tile, linear_tile_count());
+  return SARATHI_OK;
+}
+
+int sarathi_linear_tiled(int kind, int M, int N, int K, const void* x, const void* w, const void* resid, void* out,
+                         void* scratch, size_t scratch_bytes, int tile, int n_split, void* hip_stream) {
+  if (tile < 0 || tile >= linear_tile_count()) return fail(SARATHI_EINVAL, "tile %d outside [0, %d)", tile, linear_tile_count());
+  if (n_split < 1) return fail(SARATHI_EINVAL, "n_split %d < 1", n_split);
+  if (K % 64) return fail(SARATHI_EUNSUPPORTED, "K %d must be a multiple of 64 for a given tile", K);
+  return linear_common(SARATHI_BF16, kind, M, N, K, x, w, resid, out, scratch, scratch_bytes, hip_stream, tile,
+                       n_split);
 }
 
 }  // extern "C"

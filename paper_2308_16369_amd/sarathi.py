@@ -119,6 +119,11 @@ EXPORTS = {
     "sarathi_linear_scratch_bytes": (ct.c_size_t, [ct.c_int, ct.c_int]),
     "sarathi_linear": (ct.c_int, [ct.c_int, ct.c_int, ct.c_int, ct.c_int, ct.c_int, ct.c_void_p, ct.c_void_p,
                                   ct.c_void_p, ct.c_void_p, ct.c_void_p, ct.c_size_t, ct.c_void_p]),
+    "sarathi_linear_tile_count": (ct.c_int, []),
+    "sarathi_linear_tile_shape": (ct.c_int, [ct.c_int, ct.POINTER(ct.c_int), ct.POINTER(ct.c_int)]),
+    "sarathi_linear_tiled": (ct.c_int, [ct.c_int, ct.c_int, ct.c_int, ct.c_int, ct.c_void_p, ct.c_void_p,
+                                        ct.c_void_p, ct.c_void_p, ct.c_void_p, ct.c_size_t, ct.c_int, ct.c_int,
+                                        ct.c_void_p]),
     "sarathi_sched_create": (ct.c_int, [ct.POINTER(sarathi_sched_cfg), ct.POINTER(ct.c_void_p)]),
     "sarathi_sched_destroy": (None, [ct.c_void_p]),
     "sarathi_sched_submit": (ct.c_int, [ct.c_void_p, ct.c_int, ct.c_int, ct.POINTER(ct.c_int)]),
@@ -309,6 +314,24 @@ def sarathi_linear(dtype, kind, M, N, K, x: int, w: int, resid: int, out: int, s
                    scratch_bytes: int = 0, stream: int = 0, check: bool = True) -> int:
     rc = lib().sarathi_linear(dtype, kind, M, N, K, ct.c_void_p(x), ct.c_void_p(w), ct.c_void_p(resid or None),
                               ct.c_void_p(out), ct.c_void_p(scratch or None), scratch_bytes, ct.c_void_p(stream))
+    return _check(rc) if check else rc
+
+
+def sarathi_linear_tile_count() -> int:
+    return lib().sarathi_linear_tile_count()
+
+
+def sarathi_linear_tile_shape(tile: int):
+    bm, bn = ct.c_int(), ct.c_int()
+    _check(lib().sarathi_linear_tile_shape(tile, ct.byref(bm), ct.byref(bn)))
+    return bm.value, bn.value
+
+
+def sarathi_linear_tiled(kind, M, N, K, x: int, w: int, resid: int, out: int, scratch: int, scratch_bytes: int,
+                         tile: int, n_split: int, stream: int = 0, check: bool = True) -> int:
+    rc = lib().sarathi_linear_tiled(kind, M, N, K, ct.c_void_p(x), ct.c_void_p(w), ct.c_void_p(resid or None),
+                                    ct.c_void_p(out), ct.c_void_p(scratch or None), scratch_bytes, tile, n_split,
+                                    ct.c_void_p(stream))
     return _check(rc) if check else rc
 
 

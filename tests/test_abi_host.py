@@ -232,3 +232,25 @@ def test_linear_validation(lib):
     assert S.sarathi_linear(S.BF16, S.LINEAR_PLAIN, 0, 4, 16, FAKE_DEV, FAKE_DEV, 0, FAKE_DEV,
                             check=False) == S.EINVAL
     assert S.sarathi_linear_scratch_bytes(320, 5120) == 6 * 320 * 5120 * 4
+
+
+def test_linear_tile_queries_and_validation(lib):
+    n = S.sarathi_linear_tile_count()
+    assert n >= 4
+    shapes = [S.sarathi_linear_tile_shape(t) for t in range(n)]
+    assert len(set(shapes)) == n
+    for bm, bn in shapes:
+        assert bm % 16 == 0 and bn % 32 == 0
+    bm, bn = ct.c_int(), ct.c_int()
+    assert lib.sarathi_linear_tile_shape(n, ct.byref(bm), ct.byref(bn)) == S.EINVAL
+    assert lib.sarathi_linear_tile_shape(-1, ct.byref(bm), ct.byref(bn)) == S.EINVAL
+    assert lib.sarathi_linear_tile_shape(0, None, ct.byref(bn)) == S.EINVAL
+    call = lambda **kw: S.sarathi_linear_tiled(kw.get("kind", S.LINEAR_PLAIN), 4, 4, kw.get("K", 64), FAKE_DEV,
+                                               FAKE_DEV, 0, FAKE_DEV, 0, 0, kw.get("tile", 0),
+                                               kw.get("n_split", 1), check=False)
+    assert call(tile=n) == S.EINVAL
+    assert call(tile=-1) == S.EINVAL
+    assert call(n_split=0) == S.EINVAL
+    assert call(K=96) == S.EUNSUPPORTED                  # not a multiple of 64
+    assert call(kind=9) == S.EINVAL
+    assert call(kind=S.LINEAR_RESID) == S.EINVAL         # resid is NULL

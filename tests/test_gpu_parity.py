@@ -90,6 +90,49 @@ def test_linear_matches_oracle(dtype, kind, mnk):
     assert err <= TOL[dtype]
 
 
+TILE_SHAPES = [(37, 456, 1024), (200, 456, 1024)]
+
+
+@pytest.mark.parametrize("mnk", TILE_SHAPES)
+def test_linear_every_tile_shape(mnk):
+    """Every tile shape of the bf16 matmul kernel, with every epilogue (and
+    3 K-splits for the residual kinds), against the oracle on ragged shapes."""
+    M, N, K = mnk
+    n_tiles = S.sarathi_linear_tile_count()
+    rng = np.random.default_rng(M + N + K)
+    x = wl.round_to_bf16(rng.standard_normal((M, K)).astype(np.float32))
+    w = wl.round_to_bf16((rng.standard_normal((2 * N, K)) * 0.05).astype(np.float32))
+    resid = rng.standard_normal((M, N)).astype(np.float32)
+    resid_bf = wl.round_to_bf16(resid)
+    z2 = oracle.linear(x, w)
+    z = z2[:, :N]
+    xd, wd = to_dev(x, "bf16"), to_dev(w, "bf16")
+    rd_bf, rd_f32 = to_dev(resid_bf, "bf16"), torch.from_numpy(resid).cuda()
+    scratch = torch.empty(S.sarathi_linear_scratch_bytes(M, N), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    refs = {S.LINEAR_PLAIN: z, S.LINEAR_RESID: resid_bf.astype(np.float64) + z,
+            S.LINEAR_RESID_F32IN: resid.astype(np.float64) + z,
+            S.LINEAR_SWIGLU: oracle.silu(z2[:, :N]) * z2[:, N:], S.LINEAR_GELU: oracle.gelu(z)}
+    for tile in range(n_tiles):
+        for kind, ref in refs.items():
+            for n_split in ((1, 3) if kind in (S.LINEAR_RESID, S.LINEAR_RESID_F32IN) else (1,)):
+                out = torch.full((M, N), float("nan"), device="cuda",
+                                 dtype=torch.float32 if kind == S.LINEAR_RESID else torch.bfloat16)
+                rd = rd_bf if kind == S.LINEAR_RESID else rd_f32
+                S.sarathi_linear_tiled(kind, M, N, K, xd.data_ptr(), wd.data_ptr(),
+                                       rd.data_ptr() if kind in (S.LINEAR_RESID, S.LINEAR_RESID_F32IN) else 0,
+                                       out.data_ptr(), scratch.data_ptr(), scratch.numel(), tile, n_split, stream)
+                torch.cuda.synchronize()
+                got = from_dev(out)
+                err = rel_err(got, ref)
+                if kind in (S.LINEAR_RESID, S.LINEAR_RESID_F32IN):
+                    err = max(err, delta_err(got, ref, z, "f32" if kind == S.LINEAR_RESID else "bf16"))
+                label = f"tile {S.sarathi_linear_tile_shape(tile)} kind {kind} split {n_split} {mnk}"
+                log(f"{label}: err {err:.3e}")
+                assert np.all(np.isfinite(got)), label
+                assert err <= TOL["bf16"], label
+
+
 @pytest.mark.parametrize("kind", [S.LINEAR_RESID, S.LINEAR_RESID_F32IN])
 def test_linear_split_k_deterministic(kind):
     """Split-K (small M, large K) gives bit-identical results run to run, and
