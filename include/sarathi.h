@@ -178,7 +178,8 @@ int sarathi_kv_get_strides(const sarathi_kv* kv, sarathi_kv_strides* out);
  * intermediates below hold that layer's values (element offsets in bytes from
  * the workspace base):
  *   a    [T, hidden]            dtype   norm_2 output (norm_1's is overwritten)
- *   qkv  [T, 3*nh*hd]           dtype   preproj output; q columns rotated in place
+ *   qkv  [T, 3*nh*hd]           dtype   preproj output: the q columns (rotated); the k and
+ *                                       v columns are undefined (k, v go to the KV cache)
  *   o    [T, nh*hd]             dtype   attention output
  *   hres [T, hidden]            fp32    x + postproj(o)
  *   m    [T, ffn]               dtype   ffn_ln1 activation output

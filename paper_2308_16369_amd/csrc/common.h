@@ -67,6 +67,18 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// Rotary embedding: frequency of pair index i (of head_dim hd),
+// base^(-2i/hd) with lb = log2(base), in fp64; the angle pos * theta is
+// reduced to [-pi, pi] in fp64, then sin / cos in fp32.
+__device__ __forceinline__ double rope_theta(int i, int hd, double lb) {
+  return exp2(-2.0 * (double)i / (double)hd * lb);
+}
+__device__ __forceinline__ void rope_sincos(int pos, double theta, float* sn, float* cs) {
+  const double ang = (double)pos * theta;
+  const double red = ang - 6.283185307179586 * rint(ang * 0.15915494309189535);
+  __sincosf((float)red, sn, cs);
+}
+
 // KV cache element strides: [layer][slot][K|V][head][pos][head_dim].
 struct KVStrides {
   size_t layer, slot, kv, head, pos;

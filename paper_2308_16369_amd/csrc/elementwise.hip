@@ -169,12 +169,8 @@ __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
   const double lb = log2((double)a.base);
 #pragma unroll
   for (int e = 0; e < P; ++e) {
-    // angle pos * base^(-2i/hd), reduced to [-pi, pi] in fp64, sin/cos in fp32
-    const double theta = exp2(-2.0 * (double)(i0 + e) / (double)a.hd * lb);
-    const double ang = (double)pos * theta;
-    const double red = ang - 6.283185307179586 * rint(ang * 0.15915494309189535);
     float sn, c;
-    __sincosf((float)red, &sn, &c);
+    rope_sincos(pos, rope_theta(i0 + e, a.hd, lb), &sn, &c);
     const float nq0 = q0[e] * c - q1[e] * sn, nq1 = q0[e] * sn + q1[e] * c;
     const float nk0 = k0[e] * c - k1[e] * sn, nk1 = k0[e] * sn + k1[e] * c;
     q0[e] = nq0; q1[e] = nq1; k0[e] = nk0; k1[e] = nk1;

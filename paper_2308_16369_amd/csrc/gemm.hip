@@ -21,7 +21,7 @@
 namespace sarathi {
 
 enum Epi { EPI_STORE = 0, EPI_GELU = 1, EPI_SWIGLU = 2, EPI_RESID_TO_F32 = 3, EPI_RESIDF32_TO_ACT = 4,
-           EPI_PARTIAL = 5 };
+           EPI_PARTIAL = 5, EPI_ROPE_KV = 6 };
 
 struct GemmP {
   const void* A;        // [M, K]
@@ -33,6 +33,7 @@ struct GemmP {
                         // rotate their k-tile order
   void* out;            // [M, N]: dtype, or fp32 for EPI_RESID_TO_F32; EPI_PARTIAL: fp32 [n_split][M, N]
   const void* resid;    // EPI_RESID_TO_F32: dtype [M,N]; EPI_RESIDF32_TO_ACT: fp32 [M,N]
+  RopeArgs rope;        // EPI_ROPE_KV: rotary embedding + KV append of the preproj output
 };
 
 // Output element handling shared by both kernels.
@@ -245,6 +246,80 @@ __device__ __forceinline__ int w_row_of(int nl, int n0_out, int N) {
   return min(n0_out + nl, N - 1);
 }
 
+// Epilogue of preproj with the rotary embedding and the KV append fused (the
+// "others" of Sec. 2.1 that follow the QKV matmul): the block's tile (whole
+// heads of q, k or v: BN a multiple of head_dim, the [q|k|v] parts a multiple
+// of BN) goes to LDS as bf16 -- the rounding the separate kernel would read --
+// then each thread takes a row and 8 pairs (d, d + hd/2) of one head:
+// q is rotated into the output, k is rotated and v copied into the KV cache
+// at the row's (slot, position), 16 bytes per access.  The k and v columns of
+// the output are not written (attention reads them from the cache).
+template <int BM, int BN, int WGM, int WGN, int WTM, int WTN, int FM, int FN>
+__device__ __forceinline__ void rope_kv_epilogue(const GemmP& p, floatx4 (&acc)[FM][FN], int m0, int n0, int wm,
+                                                 int wn, int lane, int tid) {
+  extern __shared__ uint4 lds[];
+  bf16* t = reinterpret_cast<bf16*>(lds);                  // [BM][BN] bf16
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = wm * WTM + fm * 16 + 4 * (lane >> 4) + i;
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) t[r * BN + wn * WTN + fn * 16 + (lane & 15)] = f2bf(acc[fm][fn][i]);
+    }
+  lds_read_barrier();                                       // the producers pass their last barrier too
+  const RopeArgs& a = p.rope;
+  const int hd = a.hd, half = hd / 2, QD = a.nh * hd;
+  const int part = n0 / QD;                                 // 0 q, 1 k, 2 v
+  const int groups = half / 8;                              // 8-pair groups per head
+  const int heads = BN / hd;
+  const double lb = log2((double)a.base);
+  bf16* cache = reinterpret_cast<bf16*>(a.kv_layer);
+  // the thread's group g = tid % groups is the same for all its items (the
+  // stride is a multiple of groups): its 8 frequencies are computed once
+  static_assert((64 * WGM * WGN) % 8 == 0, "item stride");
+  double theta[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) theta[e] = rope_theta((tid % groups) * 8 + e, hd, lb);
+  for (int it = tid; it < BM * heads * groups; it += 64 * WGM * WGN) {
+    const int g = it % groups, j = (it / groups) % heads, r = it / (groups * heads);
+    const int row = m0 + r;
+    if (row >= p.M) continue;
+    const int d0 = g * 8, col = n0 + j * hd;                // first column of the head in [0, 3 QD)
+    const int head = (col % QD) / hd;
+    uint4 lo = *reinterpret_cast<const uint4*>(t + r * BN + j * hd + d0);
+    uint4 hi = *reinterpret_cast<const uint4*>(t + r * BN + j * hd + half + d0);
+    const int slot = a.row_slot[row], pos = a.row_pos[row];
+    if (part < 2 && a.rope) {
+      float x0[8], x1[8];
+      Vec16<bf16>::unpack(lo, x0);
+      Vec16<bf16>::unpack(hi, x1);
+      uint32_t w0[4], w1[4];
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        float s0, c0, s1, c1;
+        rope_sincos(pos, theta[e], &s0, &c0);
+        rope_sincos(pos, theta[e + 1], &s1, &c1);
+        const bf16 a0 = f2bf(x0[e] * c0 - x1[e] * s0), b0 = f2bf(x0[e] * s0 + x1[e] * c0);
+        const bf16 a1 = f2bf(x0[e + 1] * c1 - x1[e + 1] * s1), b1 = f2bf(x0[e + 1] * s1 + x1[e + 1] * c1);
+        w0[e / 2] = (uint32_t)a0 | ((uint32_t)a1 << 16);
+        w1[e / 2] = (uint32_t)b0 | ((uint32_t)b1 << 16);
+      }
+      lo = make_uint4(w0[0], w0[1], w0[2], w0[3]);
+      hi = make_uint4(w1[0], w1[1], w1[2], w1[3]);
+    }
+    bf16* dst;
+    if (part == 0) {
+      dst = reinterpret_cast<bf16*>(p.out) + (size_t)row * p.N + col;
+    } else {
+      dst = cache + (size_t)slot * a.st.slot + (part == 2 ? a.st.kv : 0) + (size_t)head * a.st.head +
+            (size_t)pos * a.st.pos;
+    }
+    *reinterpret_cast<uint4*>(dst + d0) = lo;
+    *reinterpret_cast<uint4*>(dst + half + d0) = hi;
+  }
+}
+
 template <int BM, int BN, int WGM, int WGN, int NP, int S, int EPI>
 __global__ __launch_bounds__(64 * (WGM * WGN + NP)) void gemm_ws_kernel(GemmP p) {
   constexpr int NC = WGM * WGN;
@@ -324,6 +399,7 @@ __global__ __launch_bounds__(64 * (WGM * WGN + NP)) void gemm_ws_kernel(GemmP p)
       lds_barrier();
       nbuf = (nbuf + 1 == S) ? 0 : nbuf + 1;
     }
+    if constexpr (EPI == EPI_ROPE_KV) lds_barrier();   // pairs with the consumers' epilogue barrier
     return;
   }
 
@@ -363,6 +439,10 @@ __global__ __launch_bounds__(64 * (WGM * WGN + NP)) void gemm_ws_kernel(GemmP p)
     buf = (buf + 1 == S) ? 0 : buf + 1;
   }
 
+  if constexpr (EPI == EPI_ROPE_KV) {
+    rope_kv_epilogue<BM, BN, WGM, WGN, WTM, WTN, FM, FN>(p, acc, m0, tile_n * BN, wm, wn, lane, tid);
+    return;
+  }
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm) {
 #pragma unroll
@@ -576,6 +656,7 @@ static hipError_t run_ws_epi(int epi, int cfg, const GemmP& p, hipStream_t s) {
     case EPI_SWIGLU: return run_ws_cfg<EPI_SWIGLU>(cfg, p, s);
     case EPI_RESID_TO_F32: return run_ws_cfg<EPI_RESID_TO_F32>(cfg, p, s);
     case EPI_RESIDF32_TO_ACT: return run_ws_cfg<EPI_RESIDF32_TO_ACT>(cfg, p, s);
+    case EPI_ROPE_KV: return run_ws_cfg<EPI_ROPE_KV>(cfg, p, s);
     default: return run_ws_cfg<EPI_PARTIAL>(cfg, p, s);
   }
 }
@@ -681,6 +762,16 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s, int forc
   const int out_per_tile = swiglu ? BN / 2 : BN;
   p.tiles_m = (a.M + BM - 1) / BM;
   p.tiles_n = (a.N + out_per_tile - 1) / out_per_tile;
+  // preproj with the rotary embedding and KV append in its epilogue when a
+  // block holds whole heads of one of q, k, v
+  if (ws && a.kind == LIN_PLAIN && a.rope != nullptr) {
+    const int hd = a.rope->hd, QD = a.rope->nh * hd;
+    if (BN % hd == 0 && QD % BN == 0 && a.N == 3 * QD) {
+      epi = EPI_ROPE_KV;
+      p.rope = *a.rope;
+      if (a.rope_done) *a.rope_done = true;
+    }
+  }
   // rotated k order pays off for two M-tiles over 128-row W panels (measured:
   // -13% on preproj at 320 rows; no gain with 256-row panels or four M-tiles)
   p.rotate_k = (ws && BN == 128 && p.tiles_m == 2) ? 1 : 0;

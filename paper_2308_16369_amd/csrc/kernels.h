@@ -50,6 +50,12 @@ struct LinearArgs {
   void* out;            // LIN_RESID: fp32 [M,N]; others dtype [M,N]
   float* parts;         // residual kinds: fp32 scratch for split-K partials (null: no split-K)
   size_t parts_cap;     // its capacity in floats
+  // LIN_PLAIN preproj (bf16), optional: rotary embedding + KV append fused
+  // into the epilogue when the tile shape allows it (then *rope_done = true,
+  // only the q columns of out are written; else the caller runs
+  // launch_rope_append).
+  const RopeArgs* rope;
+  bool* rope_done;
 };
 constexpr int MAX_SPLIT = 6;   // split-K partials: at most MAX_SPLIT x [M, N] fp32
 // force_tile >= 0 (bf16, K a multiple of 64): run that producer/consumer tile

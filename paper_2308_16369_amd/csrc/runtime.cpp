@@ -375,20 +375,25 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
   e = launch_norm(dt, false, ln, x_in, w->norm1_g, w->norm1_b, ws + c.L.a, T, H, cfg->eps, c.s);
   if (e != hipSuccess) return hip_fail(e, "norm_1");
 
-  // preproj over all rows
-  SARATHI_MARK();
-  LinearArgs q{};
-  q.kind = LIN_PLAIN; q.M = T; q.N = 3 * QD; q.K = H; q.x = ws + c.L.a; q.w = w->w_qkv; q.out = ws + c.L.qkv;
-  e = launch_linear(dt, q, c.s);
-  if (e != hipSuccess) return hip_fail(e, "preproj");
-
-  // rotary embedding + in-place KV append
+  // preproj over all rows, with the rotary embedding and the in-place KV
+  // append in its epilogue when the tile holds whole heads
   SARATHI_MARK();
   RopeArgs ra{};
   ra.qkv = ws + c.L.qkv; ra.T = T; ra.nh = nh; ra.hd = hd; ra.rope = cfg->rope; ra.base = cfg->rope_base;
   ra.row_slot = meta + P.o_slot; ra.row_pos = meta + P.o_pos; ra.kv_layer = kv_layer; ra.st = c.kv->st;
-  e = launch_rope_append(dt, ra, c.s);
-  if (e != hipSuccess) return hip_fail(e, "rope/kv append");
+  bool rope_done = false;
+  LinearArgs q{};
+  q.kind = LIN_PLAIN; q.M = T; q.N = 3 * QD; q.K = H; q.x = ws + c.L.a; q.w = w->w_qkv; q.out = ws + c.L.qkv;
+  q.rope = &ra; q.rope_done = &rope_done;
+  e = launch_linear(dt, q, c.s);
+  if (e != hipSuccess) return hip_fail(e, "preproj");
+
+  // rotary embedding + in-place KV append (unless fused above)
+  SARATHI_MARK();
+  if (!rope_done) {
+    e = launch_rope_append(dt, ra, c.s);
+    if (e != hipSuccess) return hip_fail(e, "rope/kv append");
+  }
 
   // attention: the chunk and the decodes separately, then one combine pass
   SARATHI_MARK();
