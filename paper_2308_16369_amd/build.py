@@ -17,7 +17,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libsarathi.so")
-SOURCES = ["runtime.cpp", "scheduler.cpp", "elementwise.hip", "gemm.hip", "chunk_attention.hip", "decode_attention.hip"]
+SOURCES = ["runtime.cpp", "scheduler.cpp", "elementwise.hip", "gemm.hip", "chunk_attention.hip", "decode_attention.hip",
+           "attention_combine.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

@@ -234,13 +234,9 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(PrefillArgs 
 template <int D, int NW, int S>
 static hipError_t run_prefill(const PrefillArgs& a, unsigned grid, float scale_log2, hipStream_t s) {
   const size_t lds_bytes = (size_t)S * 2 * 64 * (D / 8) * 16;
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)attn_prefill_bf16_kernel<D, NW, S>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
+  static std::atomic<uint64_t> lds_set{0};   // devices on which this instance's LDS limit is raised
+  hipError_t e = ensure_dynamic_lds((const void*)attn_prefill_bf16_kernel<D, NW, S>, (int)lds_bytes, lds_set);
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL((attn_prefill_bf16_kernel<D, NW, S>), dim3(grid), dim3(64 * NW), lds_bytes, s, a, scale_log2);
   return hipGetLastError();
 }

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
 #include <cmath>
 
 namespace sarathi {
@@ -83,6 +84,20 @@ __device__ __forceinline__ void rope_sincos(int pos, double theta, float* sn, fl
 struct KVStrides {
   size_t layer, slot, kv, head, pos;
 };
+
+// Raises a kernel's dynamic-LDS limit to `bytes` once per device (the
+// attribute belongs to the current device; `done` records the devices already
+// set, so concurrent callers may both set it, harmlessly).
+inline hipError_t ensure_dynamic_lds(const void* kernel, int bytes, std::atomic<uint64_t>& done) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const uint64_t bit = (dev >= 0 && dev < 64) ? (1ull << dev) : 0;
+  if (bit && (done.load(std::memory_order_acquire) & bit)) return hipSuccess;
+  e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (e == hipSuccess && bit) done.fetch_or(bit, std::memory_order_acq_rel);
+  return e;
+}
 
 // LDS DMA and its waits.
 typedef __attribute__((address_space(3))) void lds_void_t;

@@ -1,6 +1,7 @@
 // Attention of the decodes of the hybrid batch, run separately from the
-// prompt chunk (Sec. 4.3), and the combine pass that merges the per-split
-// partial results (max, sum, unnormalised o) of every row -- chunk rows too.
+// prompt chunk (Sec. 4.3).  It writes per-split partial results (max, sum,
+// unnormalised o) that the combine pass of attention_combine.hip merges per
+// row.
 //
 // Row attention (decodes; in fp32 runs also the chunk rows): each row attends
 // to keys 0..pos of its slot.  Work item = (row, split of split_keys keys); a
@@ -157,73 +158,6 @@ hipError_t launch_attn_rows(int dtype, const RowAttnArgs& a, hipStream_t s) {
   if (a.n_work <= 0) return hipSuccess;
   if (dtype == 0) return a.hd == 128 ? run_rows<float, 128>(a, s) : run_rows<float, 64>(a, s);
   return a.hd == 128 ? run_rows<bf16, 128>(a, s) : run_rows<bf16, 64>(a, s);
-}
-
-// ============================================================================ combine
-// O = sum_s o_s 2^(m_s - M) / sum_s l_s 2^(m_s - M), M = max_s m_s.  One wave
-// per (row, head), four heads per block: the lanes read the splits' (m, l)
-// pairs in parallel, then every lane accumulates its D/64 columns over the
-// splits with independent loads.
-template <typename T, int D>
-__global__ __launch_bounds__(256) void attn_combine_kernel(CombineArgs a) {
-  constexpr int E = D / 64;
-  const int r = blockIdx.x, lane = threadIdx.x & 63;
-  const int h = blockIdx.y * 4 + (threadIdx.x >> 6);
-  if (h >= a.nh) return;
-  const int start = a.comb[3 * r], cnt = a.comb[3 * r + 1], stride = a.comb[3 * r + 2];
-  auto src_of = [&](int j) { return a.part + ((size_t)(start + j * stride) * a.nh + h) * (D + 2); };
-  float M = -INFINITY;
-  for (int j0 = 0; j0 < cnt; j0 += 64)
-    if (j0 + lane < cnt) M = fmaxf(M, src_of(j0 + lane)[0]);
-  M = wave_max(M);
-  const float Ms = (M == -INFINITY) ? 0.f : M;
-  float L = 0.f;
-  float acc[E];
-#pragma unroll
-  for (int e = 0; e < E; ++e) acc[e] = 0.f;
-  for (int j0 = 0; j0 < cnt; j0 += 64) {
-    const int nj = min(64, cnt - j0);
-    const float* mine = src_of(j0 + min(lane, nj - 1));
-    const float wl = lane < nj ? exp2f(mine[0] - Ms) : 0.f;
-    L += wl * (lane < nj ? mine[1] : 0.f);
-    int j = 0;
-    for (; j + 4 <= nj; j += 4) {
-      float v[4][E];
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int e = 0; e < E; ++e) v[u][e] = src_of(j0 + j + u)[2 + lane + 64 * e];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const float w = __shfl(wl, j + u, 64);
-#pragma unroll
-        for (int e = 0; e < E; ++e) acc[e] = fmaf(v[u][e], w, acc[e]);
-      }
-    }
-    for (; j < nj; ++j) {
-      const float w = __shfl(wl, j, 64);
-#pragma unroll
-      for (int e = 0; e < E; ++e) acc[e] = fmaf(src_of(j0 + j)[2 + lane + 64 * e], w, acc[e]);
-    }
-  }
-  L = wave_sum(L);
-  const float inv = 1.0f / L;
-  T* out = reinterpret_cast<T*>(a.out) + (size_t)r * a.ld_out + h * D;
-#pragma unroll
-  for (int e = 0; e < E; ++e) out[lane + 64 * e] = from_f<T>(acc[e] * inv);
-}
-
-hipError_t launch_attn_combine(int dtype, const CombineArgs& a, hipStream_t s) {
-  if (a.n_rows <= 0) return hipSuccess;
-  dim3 grid(a.n_rows, (a.nh + 3) / 4);
-  if (dtype == 0) {
-    if (a.hd == 128) hipLaunchKernelGGL((attn_combine_kernel<float, 128>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((attn_combine_kernel<float, 64>), grid, dim3(256), 0, s, a);
-  } else {
-    if (a.hd == 128) hipLaunchKernelGGL((attn_combine_kernel<bf16, 128>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((attn_combine_kernel<bf16, 64>), grid, dim3(256), 0, s, a);
-  }
-  return hipGetLastError();
 }
 
 }  // namespace sarathi

@@ -547,13 +547,9 @@ enum TileCfg { CFG_160x128 = 0, CFG_320x128 = 1, CFG_64x128 = 2, CFG_96x128 = 3 
 template <int BM, int BN, int WGM, int WGN, int PD, int EPI>
 static hipError_t run_bf16(GemmP p, hipStream_t s) {
   const size_t lds_bytes = 2 * (BM + BN) * 8 * sizeof(uint4);
-  static bool attr_set = false;   // the attribute is per kernel function
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)gemm_bf16_kernel<BM, BN, WGM, WGN, PD, EPI>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
+  static std::atomic<uint64_t> lds_set{0};   // devices on which this instance's LDS limit is raised
+  hipError_t e = ensure_dynamic_lds((const void*)gemm_bf16_kernel<BM, BN, WGM, WGN, PD, EPI>, (int)lds_bytes, lds_set);
+  if (e != hipSuccess) return e;
   const int grid = (p.n_tiles + 7) / 8 * 8;
   hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WGM, WGN, PD, EPI>), dim3(grid), dim3(64 * WGM * WGN), lds_bytes,
                      s, p);
@@ -563,13 +559,9 @@ static hipError_t run_bf16(GemmP p, hipStream_t s) {
 template <int BM, int BN, int WGM, int WGN, int NP, int S, int EPI>
 static hipError_t run_ws(GemmP p, hipStream_t s) {
   const size_t lds_bytes = (size_t)S * (BM + BN) * 8 * sizeof(uint4);
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)gemm_ws_kernel<BM, BN, WGM, WGN, NP, S, EPI>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
+  static std::atomic<uint64_t> lds_set{0};   // devices on which this instance's LDS limit is raised
+  hipError_t e = ensure_dynamic_lds((const void*)gemm_ws_kernel<BM, BN, WGM, WGN, NP, S, EPI>, (int)lds_bytes, lds_set);
+  if (e != hipSuccess) return e;
   const int grid = (p.n_tiles + 7) / 8 * 8;
   hipLaunchKernelGGL((gemm_ws_kernel<BM, BN, WGM, WGN, NP, S, EPI>), dim3(grid), dim3(64 * (WGM * WGN + NP)),
                      lds_bytes, s, p);
