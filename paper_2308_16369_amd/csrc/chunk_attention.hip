@@ -1,6 +1,6 @@
 // Attention of the prompt chunk(s) of the hybrid batch, run separately from the
 // decodes (Sec. 4.3).  It writes per-split partial results (max, sum,
-// unnormalised o) that the combine pass of decode_attention.hip merges per row.
+// unnormalised o) that the combine pass of attention_combine.hip merges per row.
 //
 // Chunked-prefill attention (bf16, MFMA): the chunk's queries at positions
 // off..off+C-1 attend to the prefill slot's keys 0..position (the earlier
@@ -50,9 +50,10 @@ __device__ __forceinline__ uint2 lds_read_tr16(const void* p) {
 // an S-stage LDS ring filled by LDS DMA (global_load_lds_dwordx4: a wave
 // instruction fills 1 KB = 1024 / (2 D) key rows; lane i takes LDS slot i of
 // its row and so reads the chunk that the swizzle puts there), S - 1 tiles in
-// flight while one is used; one barrier per tile.
+// flight while one is used; one barrier per tile.  Registers are capped at
+// 128 per lane (four waves per SIMD) so that two blocks share a CU.
 template <int D, int NW, int S>
-__global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(PrefillArgs a, float scale_log2) {
+__global__ __launch_bounds__(64 * NW, 4) void attn_prefill_bf16_kernel(PrefillArgs a, float scale_log2) {
   constexpr int QB = 16 * NW;            // the block's queries (chunk rows)
   constexpr int KT = 64;                 // keys per tile
   constexpr int DCH = D / 8;             // 16-byte chunks per K/V row

@@ -5,8 +5,18 @@
 namespace sarathi {
 
 // ------------------------------------------------------------------ metadata
-__global__ void meta_write_kernel(MetaChunk c, int* dst) {
-  for (int i = threadIdx.x; i < c.count; i += blockDim.x) dst[i] = c.values[i];
+// All loads of a thread are issued before its stores, so the copy costs one
+// round trip to the argument buffer rather than one per value.
+__global__ __launch_bounds__(256) void meta_write_kernel(MetaChunk c, int* dst) {
+  constexpr int PER = (META_CHUNK + 255) / 256;
+  int v[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) v[j] = c.values[min((int)threadIdx.x + 256 * j, META_CHUNK - 1)];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int i = threadIdx.x + 256 * j;
+    if (i < c.count) dst[i] = v[j];
+  }
 }
 
 hipError_t launch_meta_write(const MetaChunk& chunk, int* dst, hipStream_t s) {
@@ -44,28 +54,38 @@ template <> struct Store16<float> {
   }
 };
 
-constexpr int NORM_NC = 12;   // units per thread
+constexpr int NORM_NC = 12;   // most units per thread
 
 // A unit is CE = max(16 bytes of input, 16 bytes of output) elements, so
-// loads and stores are whole 16-byte vectors; H up to NORM_NC * 256 * CE.
-template <typename Tin, typename Tout, bool LAYER>
-__global__ __launch_bounds__(256) void norm_kernel(const Tin* __restrict__ in, const Tout* __restrict__ g,
-                                                   const Tout* __restrict__ b, Tout* __restrict__ out, int H,
-                                                   float eps) {
+// loads and stores are whole 16-byte vectors; H up to NC * 256 * CE, NC the
+// units per thread of the instance (registers scale with NC, so the launch
+// takes the smallest instance that holds the row).
+template <typename Tin, typename Tout, bool LAYER, int NC>
+__device__ __forceinline__ void norm_row(const Tin* __restrict__ in, const Tout* __restrict__ g,
+                                         const Tout* __restrict__ b, Tout* __restrict__ out, int H, float eps,
+                                         size_t row) {
   __shared__ float red[4];
   constexpr int EI = Vec16<Tin>::N, EO = Vec16<Tout>::N;
   constexpr int CE = EI > EO ? EI : EO;
-  const size_t row = blockIdx.x;
+  constexpr int GV = CE / EO;                 // 16-byte gain vectors per unit
   const Tin* x = in + row * (size_t)H;
   const int nunit = H / CE;
-  float v[NORM_NC][CE];
+  float v[NC][CE];
+  // gains (and biases) are loaded up front, beside the row, so that the
+  // output pass waits on no load
+  uint4 graw[NC][GV], braw[LAYER ? NC : 1][GV];
   float s = 0.f;
 #pragma unroll
-  for (int j = 0; j < NORM_NC; ++j) {
+  for (int j = 0; j < NC; ++j) {
     const int u = threadIdx.x + 256 * j;
     if (u < nunit) {
 #pragma unroll
       for (int o = 0; o < CE; o += EI) Vec16<Tin>::unpack(*reinterpret_cast<const uint4*>(x + u * CE + o), &v[j][o]);
+#pragma unroll
+      for (int k = 0; k < GV; ++k) {
+        graw[j][k] = *reinterpret_cast<const uint4*>(g + u * CE + k * EO);
+        if (LAYER) braw[LAYER ? j : 0][k] = *reinterpret_cast<const uint4*>(b + u * CE + k * EO);
+      }
 #pragma unroll
       for (int e = 0; e < CE; ++e) s += v[j][e];
     } else {
@@ -77,7 +97,7 @@ __global__ __launch_bounds__(256) void norm_kernel(const Tin* __restrict__ in, c
   if (LAYER) mean = block_sum_256(s, red) / (float)H;
   float ss = 0.f;
 #pragma unroll
-  for (int j = 0; j < NORM_NC; ++j) {
+  for (int j = 0; j < NC; ++j) {
     if (threadIdx.x + 256 * j < nunit) {
 #pragma unroll
       for (int e = 0; e < CE; ++e) {
@@ -89,15 +109,16 @@ __global__ __launch_bounds__(256) void norm_kernel(const Tin* __restrict__ in, c
   const float r = 1.0f / sqrtf(block_sum_256(ss, red) / (float)H + eps);
   Tout* y = out + row * (size_t)H;
 #pragma unroll
-  for (int j = 0; j < NORM_NC; ++j) {
+  for (int j = 0; j < NC; ++j) {
     const int u = threadIdx.x + 256 * j;
     if (u >= nunit) continue;
     const int i0 = u * CE;
 #pragma unroll
-    for (int o = 0; o < CE; o += EO) {
+    for (int k = 0; k < GV; ++k) {
+      const int o = k * EO;
       float gv[EO], bv[EO], f[EO];
-      Vec16<Tout>::unpack(*reinterpret_cast<const uint4*>(g + i0 + o), gv);
-      if (LAYER) Vec16<Tout>::unpack(*reinterpret_cast<const uint4*>(b + i0 + o), bv);
+      Vec16<Tout>::unpack(graw[j][k], gv);
+      if (LAYER) Vec16<Tout>::unpack(braw[LAYER ? j : 0][k], bv);
 #pragma unroll
       for (int e = 0; e < EO; ++e) f[e] = (v[j][o + e] - mean) * r * gv[e] + (LAYER ? bv[e] : 0.f);
       *reinterpret_cast<uint4*>(y + i0 + o) = Store16<Tout>::pack(f);
@@ -105,26 +126,77 @@ __global__ __launch_bounds__(256) void norm_kernel(const Tin* __restrict__ in, c
   }
 }
 
-template <typename Tin, typename Tout>
-static void norm_dispatch(bool layer, const void* in, const void* g, const void* b, void* out, int rows, int H,
-                          float eps, hipStream_t s) {
-  if (layer)
-    hipLaunchKernelGGL((norm_kernel<Tin, Tout, true>), dim3(rows), dim3(256), 0, s, (const Tin*)in,
-                       (const Tout*)g, (const Tout*)b, (Tout*)out, H, eps);
+template <typename Tin, typename Tout, bool LAYER, int NC>
+__global__ __launch_bounds__(256) void norm_kernel(const Tin* __restrict__ in, const Tout* __restrict__ g,
+                                                   const Tout* __restrict__ b, Tout* __restrict__ out, int H,
+                                                   float eps) {
+  norm_row<Tin, Tout, LAYER, NC>(in, g, b, out, H, eps, blockIdx.x);
+}
+
+// The first norm of a layer call with the metadata upload riding along:
+// block 0 copies the metadata chunk (as meta_write_kernel), blocks 1..rows
+// normalise rows 0..rows-1.  One launch instead of two.
+template <typename Tin, typename Tout, bool LAYER, int NC>
+__global__ __launch_bounds__(256) void norm_meta_kernel(const Tin* __restrict__ in, const Tout* __restrict__ g,
+                                                        const Tout* __restrict__ b, Tout* __restrict__ out, int H,
+                                                        float eps, MetaChunk c, int* __restrict__ dst) {
+  if (blockIdx.x == 0) {
+    constexpr int PER = (META_CHUNK + 255) / 256;
+    int v[PER];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) v[j] = c.values[min((int)threadIdx.x + 256 * j, META_CHUNK - 1)];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int i = threadIdx.x + 256 * j;
+      if (i < c.count) dst[i] = v[j];
+    }
+    return;
+  }
+  norm_row<Tin, Tout, LAYER, NC>(in, g, b, out, H, eps, blockIdx.x - 1);
+}
+
+template <typename Tin, typename Tout, bool LAYER, int NC>
+static void norm_launch_nc(const void* in, const void* g, const void* b, void* out, int rows, int H, float eps,
+                           hipStream_t s, const MetaChunk* meta, int* meta_dst) {
+  if (meta)
+    hipLaunchKernelGGL((norm_meta_kernel<Tin, Tout, LAYER, NC>), dim3(rows + 1), dim3(256), 0, s, (const Tin*)in,
+                       (const Tout*)g, (const Tout*)b, (Tout*)out, H, eps, *meta, meta_dst);
   else
-    hipLaunchKernelGGL((norm_kernel<Tin, Tout, false>), dim3(rows), dim3(256), 0, s, (const Tin*)in,
+    hipLaunchKernelGGL((norm_kernel<Tin, Tout, LAYER, NC>), dim3(rows), dim3(256), 0, s, (const Tin*)in,
                        (const Tout*)g, (const Tout*)b, (Tout*)out, H, eps);
 }
 
+template <typename Tin, typename Tout, bool LAYER>
+static void norm_launch(const void* in, const void* g, const void* b, void* out, int rows, int H, float eps,
+                        hipStream_t s, const MetaChunk* meta, int* meta_dst) {
+  constexpr int EI = Vec16<Tin>::N, EO = Vec16<Tout>::N;
+  constexpr int CE = EI > EO ? EI : EO;
+  const int nc = (H / CE + 255) / 256;
+  if (nc <= 2) norm_launch_nc<Tin, Tout, LAYER, 2>(in, g, b, out, rows, H, eps, s, meta, meta_dst);
+  else if (nc <= 4) norm_launch_nc<Tin, Tout, LAYER, 4>(in, g, b, out, rows, H, eps, s, meta, meta_dst);
+  else if (nc <= 6) norm_launch_nc<Tin, Tout, LAYER, 6>(in, g, b, out, rows, H, eps, s, meta, meta_dst);
+  else norm_launch_nc<Tin, Tout, LAYER, NORM_NC>(in, g, b, out, rows, H, eps, s, meta, meta_dst);
+}
+
+template <typename Tin, typename Tout>
+static void norm_dispatch(bool layer, const void* in, const void* g, const void* b, void* out, int rows, int H,
+                          float eps, hipStream_t s, const MetaChunk* meta, int* meta_dst) {
+  if (layer)
+    norm_launch<Tin, Tout, true>(in, g, b, out, rows, H, eps, s, meta, meta_dst);
+  else
+    norm_launch<Tin, Tout, false>(in, g, b, out, rows, H, eps, s, meta, meta_dst);
+}
+
 hipError_t launch_norm(int dtype, bool in_f32, bool layer_norm, const void* in, const void* g,
-                       const void* b, void* out, int rows, int H, float eps, hipStream_t s) {
+                       const void* b, void* out, int rows, int H, float eps, hipStream_t s,
+                       const MetaChunk* meta, int* meta_dst) {
   if (rows <= 0) return hipSuccess;
   if (dtype == 0)
-    norm_dispatch<float, float>(layer_norm, in, g, b, out, rows, H, eps, s);
+    norm_dispatch<float, float>(layer_norm, in, g, b, out, rows, H, eps, s, meta, meta_dst);
   else if (in_f32)
-    norm_dispatch<float, bf16>(layer_norm, in, g, b, out, rows, H, eps, s);
+    norm_dispatch<float, bf16>(layer_norm, in, g, b, out, rows, H, eps, s, meta, meta_dst);
   else
-    norm_dispatch<bf16, bf16>(layer_norm, in, g, b, out, rows, H, eps, s);
+    norm_dispatch<bf16, bf16>(layer_norm, in, g, b, out, rows, H, eps, s, meta, meta_dst);
   return hipGetLastError();
 }
 

@@ -23,8 +23,11 @@ struct MetaChunk {
 hipError_t launch_meta_write(const MetaChunk& chunk, int* dst, hipStream_t s);
 
 // ---- norms (one row per block).  in: [rows, H] of Tin; out: [rows, H] of dtype.
+// With meta non-null the same launch also copies that metadata chunk to
+// meta_dst (one extra block).
 hipError_t launch_norm(int dtype, bool in_f32, bool layer_norm, const void* in, const void* g,
-                       const void* b, void* out, int rows, int H, float eps, hipStream_t s);
+                       const void* b, void* out, int rows, int H, float eps, hipStream_t s,
+                       const MetaChunk* meta = nullptr, int* meta_dst = nullptr);
 
 // ---- rotary embedding of q, k in place of the preproj output and K/V append.
 struct RopeArgs {

@@ -227,9 +227,9 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
     // QBLOCK partial rows apart); the work items run split by split so that
     // the query blocks that read the same keys are neighbours (and share an
     // XCD's L2, see the chunk-attention kernel).
-    // Key split: the largest (PRE_SPLIT x 2^j) that still gives every CU a
-    // block (fewer, longer items write fewer partials); PRE_SPLIT when even
-    // that leaves CUs idle.
+    // Key split: the largest (PRE_SPLIT x 2^j) that still fills both block
+    // slots of every CU (two blocks run per CU; fewer, longer items write
+    // fewer partials); PRE_SPLIT when even that leaves slots idle.
     auto n_blocks = [&](int split) {
       long n = 0;
       for (const ChunkDesc& c : b.chunks)
@@ -238,7 +238,7 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
       return n * cfg->n_heads;
     };
     p.pre_split = PRE_SPLIT;
-    while (p.pre_split < (1 << 20) && n_blocks(2 * p.pre_split) >= 256) p.pre_split *= 2;
+    while (p.pre_split < (1 << 20) && n_blocks(2 * p.pre_split) >= 512) p.pre_split *= 2;
     const int split = p.pre_split;
     r0 = 0;
     int slot_base = 0;
@@ -333,21 +333,30 @@ struct Ctx {
   hipStream_t s;
 };
 
-int upload_meta(const Ctx& c) {
+// Metadata chunk `i` (META_CHUNK ints each).
+void meta_chunk(const Plan& p, size_t i, MetaChunk* chunk) {
+  const size_t at = i * META_CHUNK;
+  chunk->count = (int)std::min<size_t>(META_CHUNK, p.meta.size() - at);
+  std::memcpy(chunk->values, p.meta.data() + at, chunk->count * sizeof(int));
+}
+
+// Uploads every metadata chunk but the first, which the first norm_1 launch
+// of the call carries (nothing the chunks feed runs before that norm ends).
+int upload_meta_rest(const Ctx& c) {
   int* dst = reinterpret_cast<int*>(c.ws + c.L.meta);
-  const std::vector<int>& m = c.plan->meta;
-  for (size_t at = 0; at < m.size(); at += META_CHUNK) {
+  const size_t n = (c.plan->meta.size() + META_CHUNK - 1) / META_CHUNK;
+  for (size_t i = 1; i < n; ++i) {
     MetaChunk chunk;
-    chunk.count = (int)std::min<size_t>(META_CHUNK, m.size() - at);
-    std::memcpy(chunk.values, m.data() + at, chunk.count * sizeof(int));
-    hipError_t e = launch_meta_write(chunk, dst + at, c.s);
+    meta_chunk(*c.plan, i, &chunk);
+    hipError_t e = launch_meta_write(chunk, dst + i * META_CHUNK, c.s);
     if (e != hipSuccess) return hip_fail(e, "metadata upload");
   }
   return SARATHI_OK;
 }
 
 // One decoder layer; metadata already on the device.
-int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const void* x_in, void* x_out) {
+int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const void* x_in, void* x_out,
+               bool carry_meta) {
   const sarathi_model_cfg* cfg = c.cfg;
   const Plan& P = *c.plan;
   const int T = P.T, H = cfg->hidden, nh = cfg->n_heads, hd = cfg->head_dim, F = cfg->ffn;
@@ -372,7 +381,14 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
 
   // norm_1
   SARATHI_MARK();
-  e = launch_norm(dt, false, ln, x_in, w->norm1_g, w->norm1_b, ws + c.L.a, T, H, cfg->eps, c.s);
+  if (carry_meta) {
+    MetaChunk first;
+    meta_chunk(P, 0, &first);
+    e = launch_norm(dt, false, ln, x_in, w->norm1_g, w->norm1_b, ws + c.L.a, T, H, cfg->eps, c.s, &first,
+                    reinterpret_cast<int*>(ws + c.L.meta));
+  } else {
+    e = launch_norm(dt, false, ln, x_in, w->norm1_g, w->norm1_b, ws + c.L.a, T, H, cfg->eps, c.s);
+  }
   if (e != hipSuccess) return hip_fail(e, "norm_1");
 
   // preproj over all rows, with the rotary embedding and the in-place KV
@@ -570,9 +586,9 @@ int run_layer(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, sara
   if (rc) return rc;
   if (layer < 0 || layer >= cfg->n_layers) return fail(SARATHI_EINVAL, "layer %d outside [0, %d)", layer, cfg->n_layers);
   Ctx c{cfg, kv, &plan, L, static_cast<char*>(ws), static_cast<hipStream_t>(hip_stream)};
-  rc = upload_meta(c);
+  rc = upload_meta_rest(c);
   if (rc) return rc;
-  return layer_body(c, w, layer, x_in, x_out);
+  return layer_body(c, w, layer, x_in, x_out, true);
 }
 
 int run_model(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, sarathi_kv* kv, const BatchDesc& b,
@@ -582,14 +598,14 @@ int run_model(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, sara
   int rc = prepare(cfg, w, cfg->n_layers > 0 ? cfg->n_layers : 0, kv, b, x_in, x_out, ws, ws_bytes, &plan, &L);
   if (rc) return rc;
   Ctx c{cfg, kv, &plan, L, static_cast<char*>(ws), static_cast<hipStream_t>(hip_stream)};
-  rc = upload_meta(c);
+  rc = upload_meta_rest(c);
   if (rc) return rc;
   char* ping[2] = {c.ws + L.ping0, c.ws + L.ping1};
   const int n = cfg->n_layers;
   for (int l = 0; l < n; ++l) {
     const void* in = (l == 0) ? x_in : ping[l & 1];
     void* out = (l == n - 1) ? x_out : ping[(l + 1) & 1];
-    rc = layer_body(c, w + l, l, in, out);
+    rc = layer_body(c, w + l, l, in, out, l == 0);
     if (rc) return rc;
   }
   return SARATHI_OK;
