@@ -215,6 +215,20 @@ def test_layer_head_dim_128_tiny_bf16():
     run_and_check(wl.make_instance(shape, b, max_seq_len=512, n_slots=4, seed=5), "hd128 tiny bf16")
 
 
+@pytest.mark.parametrize("dtype,hidden,norm", [("bf16", 24576, "rms"), ("bf16", 12296, "layer"), ("bf16", 4104, "rms"),
+                                               ("f32", 12288, "layer"), ("f32", 1032, "rms")])
+def test_layer_wide_hidden(dtype, hidden, norm):
+    """Rows as wide as the configuration accepts (the norms keep a row in
+    registers; the register footprint is picked from the row width), plus
+    widths just past a size step, for RMSNorm and LayerNorm."""
+    shape = _tiny_shape(dtype, hidden=hidden, n_heads=2, head_dim=64, ffn=256, norm=norm,
+                        act="gelu" if norm == "layer" else "swiglu", rope=norm == "rms",
+                        eps=1e-5 if norm == "layer" else 1e-6)
+    b = wl.Batch(prefill_slot=0, chunk_offset=9, chunk_len=5, decode_slots=np.array([1, 2], np.int32),
+                 decode_ctx=np.array([3, 40], np.int32))
+    run_and_check(wl.make_instance(shape, b, max_seq_len=64, n_slots=3, seed=17), f"wide hidden {hidden} {norm}")
+
+
 @pytest.mark.parametrize("C,off,decodes", [(2048, 0, []), (1000, 2048, [(0, 3047), (2, 17)])])
 def test_layer_long_chunk_bf16(C, off, decodes):
     """Chunks as long as the full prefills of the chunk-size ablation (a
