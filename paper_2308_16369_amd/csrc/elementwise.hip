@@ -190,7 +190,7 @@ static void norm_dispatch(bool layer, const void* in, const void* g, const void*
 hipError_t launch_norm(int dtype, bool in_f32, bool layer_norm, const void* in, const void* g,
                        const void* b, void* out, int rows, int H, float eps, hipStream_t s,
                        const MetaChunk* meta, int* meta_dst) {
-  if (rows <= 0) return hipSuccess;
+  if (rows <= 0) return meta ? launch_meta_write(*meta, meta_dst, s) : hipSuccess;
   if (dtype == 0)
     norm_dispatch<float, float>(layer_norm, in, g, b, out, rows, H, eps, s, meta, meta_dst);
   else if (in_f32)
@@ -273,18 +273,29 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const Tr* __restrict_
                                                            int n_split, size_t n, To* __restrict__ out) {
   const size_t nv = n / V;
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < nv; i += (size_t)gridDim.x * blockDim.x) {
+    // every split's partial is loaded before the first add (one memory
+    // round trip, not n_split), then added in split order
+    float q[MAX_SPLIT][V];
+#pragma unroll
+    for (int sp = 0; sp < MAX_SPLIT; ++sp) {
+      if (sp >= n_split) break;
+      const float* pp = parts + (size_t)sp * n + i * V;
+      if constexpr (V == 4) {
+        const float4 f = *reinterpret_cast<const float4*>(pp);
+        q[sp][0] = f.x; q[sp][1] = f.y; q[sp][2] = f.z; q[sp][3] = f.w;
+      } else {
+#pragma unroll
+        for (int e = 0; e < V; ++e) q[sp][e] = pp[e];
+      }
+    }
     float acc[V];
 #pragma unroll
     for (int e = 0; e < V; ++e) acc[e] = to_f<Tr>(resid[i * V + e]);
-    for (int sp = 0; sp < n_split; ++sp) {
-      const float* pp = parts + (size_t)sp * n + i * V;
-      if constexpr (V == 4) {
-        const float4 q = *reinterpret_cast<const float4*>(pp);
-        acc[0] += q.x; acc[1] += q.y; acc[2] += q.z; acc[3] += q.w;
-      } else {
 #pragma unroll
-        for (int e = 0; e < V; ++e) acc[e] += pp[e];
-      }
+    for (int sp = 0; sp < MAX_SPLIT; ++sp) {
+      if (sp >= n_split) break;
+#pragma unroll
+      for (int e = 0; e < V; ++e) acc[e] += q[sp][e];
     }
 #pragma unroll
     for (int e = 0; e < V; ++e) out[i * V + e] = from_f<To>(acc[e]);
@@ -308,6 +319,7 @@ static void split_reduce_dispatch(const void* resid, const float* parts, int n_s
 hipError_t launch_split_reduce(int dtype, bool resid_f32, bool out_f32, const void* resid, const float* parts,
                                int n_split, size_t n, void* out, hipStream_t s) {
   if (n == 0) return hipSuccess;
+  if (n_split < 1 || n_split > MAX_SPLIT) return hipErrorInvalidValue;
   if (dtype == 0 || (resid_f32 && out_f32))
     split_reduce_dispatch<float, float>(resid, parts, n_split, n, out, s);
   else if (resid_f32)
