@@ -16,6 +16,14 @@ namespace sarathi {
 
 constexpr float LOG2E = 1.4426950408889634f;
 
+// 16-byte load with the non-temporal hint (streamed data, read once).
+typedef unsigned int u32x4_nt __attribute__((ext_vector_type(4)));
+template <typename T>
+__device__ __forceinline__ uint4 load_stream16(const T* p) {
+  const u32x4_nt v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_nt*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 // ============================================================================ row attention
 template <typename T, int D, int DUP>
 __global__ __launch_bounds__(256) void attn_rows_kernel(RowAttnArgs a, float scale_log2) {
@@ -57,15 +65,20 @@ __global__ __launch_bounds__(256) void attn_rows_kernel(RowAttnArgs a, float sca
   // Each wave takes passes of KP keys (pb, pb + 4*KP, ...).  All K loads are
   // issued first, then all V loads: the scores wait only for K (loads
   // complete in order) while V is still in flight.  Key addresses past the
-  // split are clamped to its last key (finite data, masked below).
+  // split are clamped to its last key (finite data, masked below).  The KV
+  // is read once per call, so its loads are non-temporal: they do not
+  // allocate in the memory-side cache, which neither evicts what other
+  // kernels left there nor forces the write-back of their dirty lines in the
+  // middle of this stream (measured: 12% faster alone, and 32-128 MB of
+  // writes by the kernel before it no longer slow it down).
   for (int pb = kb + wave * KP; pb < ke; pb += 4 * KP) {
     uint4 kr[NI], vr[NI];
 #pragma unroll
     for (int i = 0; i < NI; ++i)
-      kr[i] = *reinterpret_cast<const uint4*>(kbase + (size_t)min(pb + i * KPI + g, ke - 1) * a.st.pos);
+      kr[i] = load_stream16(kbase + (size_t)min(pb + i * KPI + g, ke - 1) * a.st.pos);
 #pragma unroll
     for (int i = 0; i < NI; ++i)
-      vr[i] = *reinterpret_cast<const uint4*>(vbase + (size_t)min(pb + i * KPI + g, ke - 1) * a.st.pos);
+      vr[i] = load_stream16(vbase + (size_t)min(pb + i * KPI + g, ke - 1) * a.st.pos);
     // Keep all 2*NI loads in flight before any use (the scheduler would
     // otherwise sink each load next to its first use and serialise them).
     __builtin_amdgcn_sched_barrier(0);
