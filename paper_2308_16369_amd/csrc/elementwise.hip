@@ -316,6 +316,109 @@ static void split_reduce_dispatch(const void* resid, const float* parts, int n_s
                        n_split, n, (To*)out);
 }
 
+// Split-K reduction of rows of N (bf16 residual, fp32 out) followed by the
+// norm of each row, one block per row: the row's sums stay in registers
+// between the reduction and the norm, so the norm reads nothing back.  The
+// sums are formed in split order as in split_reduce_kernel, and the norm
+// accumulates over the same units in the same order as norm_row, so both
+// outputs are bit-identical to the two separate passes.
+template <bool LAYER, int NC>
+__global__ __launch_bounds__(256) void split_reduce_norm_kernel(const bf16* __restrict__ resid,
+                                                                const float* __restrict__ parts, int n_split, int N,
+                                                                float* __restrict__ out, const bf16* __restrict__ g,
+                                                                const bf16* __restrict__ b, bf16* __restrict__ nout,
+                                                                float eps) {
+  __shared__ float red[4];
+  constexpr int CE = 8;                       // elements per unit: 16 bytes of bf16, 2 x 16 of fp32
+  const size_t row = blockIdx.x;
+  const size_t n = (size_t)gridDim.x * N;     // elements per split
+  const int nunit = N / CE;
+  float v[NC][CE];
+  uint4 graw[NC], braw[LAYER ? NC : 1];
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < NC; ++j) {
+    const int u = threadIdx.x + 256 * j;
+    if (u < nunit) {
+      const size_t at = row * N + (size_t)u * CE;
+      float q[MAX_SPLIT][CE];
+#pragma unroll
+      for (int sp = 0; sp < MAX_SPLIT; ++sp) {
+        if (sp >= n_split) break;
+        const float4* pp = reinterpret_cast<const float4*>(parts + (size_t)sp * n + at);
+        const float4 lo = pp[0], hi = pp[1];
+        q[sp][0] = lo.x; q[sp][1] = lo.y; q[sp][2] = lo.z; q[sp][3] = lo.w;
+        q[sp][4] = hi.x; q[sp][5] = hi.y; q[sp][6] = hi.z; q[sp][7] = hi.w;
+      }
+      graw[j] = *reinterpret_cast<const uint4*>(g + (size_t)u * CE);
+      if (LAYER) braw[LAYER ? j : 0] = *reinterpret_cast<const uint4*>(b + (size_t)u * CE);
+      Vec16<bf16>::unpack(*reinterpret_cast<const uint4*>(resid + at), v[j]);
+#pragma unroll
+      for (int sp = 0; sp < MAX_SPLIT; ++sp) {
+        if (sp >= n_split) break;
+#pragma unroll
+        for (int e = 0; e < CE; ++e) v[j][e] += q[sp][e];
+      }
+      float4* op = reinterpret_cast<float4*>(out + at);
+      op[0] = make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
+      op[1] = make_float4(v[j][4], v[j][5], v[j][6], v[j][7]);
+#pragma unroll
+      for (int e = 0; e < CE; ++e) s += v[j][e];
+    } else {
+#pragma unroll
+      for (int e = 0; e < CE; ++e) v[j][e] = 0.f;
+    }
+  }
+  float mean = 0.f;
+  if (LAYER) mean = block_sum_256(s, red) / (float)N;
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < NC; ++j) {
+    if (threadIdx.x + 256 * j < nunit) {
+#pragma unroll
+      for (int e = 0; e < CE; ++e) {
+        const float d = v[j][e] - mean;
+        ss += d * d;
+      }
+    }
+  }
+  const float r = 1.0f / sqrtf(block_sum_256(ss, red) / (float)N + eps);
+  bf16* y = nout + row * (size_t)N;
+#pragma unroll
+  for (int j = 0; j < NC; ++j) {
+    const int u = threadIdx.x + 256 * j;
+    if (u >= nunit) continue;
+    float gv[CE], bv[CE], f[CE];
+    Vec16<bf16>::unpack(graw[j], gv);
+    if (LAYER) Vec16<bf16>::unpack(braw[LAYER ? j : 0], bv);
+#pragma unroll
+    for (int e = 0; e < CE; ++e) f[e] = (v[j][e] - mean) * r * gv[e] + (LAYER ? bv[e] : 0.f);
+    *reinterpret_cast<uint4*>(y + (size_t)u * CE) = Store16<bf16>::pack(f);
+  }
+}
+
+template <bool LAYER>
+static hipError_t split_reduce_norm_layer(const void* resid, const float* parts, int n_split, int rows, int N,
+                                          float* out, const NormArgs& nm, hipStream_t s) {
+  const int nc = (N / 8 + 255) / 256;
+#define SRN_LAUNCH(NCV)                                                                                        \
+  hipLaunchKernelGGL((split_reduce_norm_kernel<LAYER, NCV>), dim3(rows), dim3(256), 0, s, (const bf16*)resid, parts, \
+                     n_split, N, out, (const bf16*)nm.g, (const bf16*)nm.b, (bf16*)nm.out, nm.eps)
+  if (nc <= 4) SRN_LAUNCH(4);
+  else if (nc <= 8) SRN_LAUNCH(8);
+  else SRN_LAUNCH(12);
+#undef SRN_LAUNCH
+  return hipGetLastError();
+}
+
+hipError_t launch_split_reduce_norm(const void* resid, const float* parts, int n_split, int rows, int N, float* out,
+                                    const NormArgs& norm, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (N % 8 != 0 || N / 8 > 12 * 256 || n_split < 1 || n_split > MAX_SPLIT) return hipErrorNotSupported;
+  return norm.layer ? split_reduce_norm_layer<true>(resid, parts, n_split, rows, N, out, norm, s)
+                    : split_reduce_norm_layer<false>(resid, parts, n_split, rows, N, out, norm, s);
+}
+
 hipError_t launch_split_reduce(int dtype, bool resid_f32, bool out_f32, const void* resid, const float* parts,
                                int n_split, size_t n, void* out, hipStream_t s) {
   if (n == 0) return hipSuccess;

@@ -803,9 +803,15 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s, int forc
     }
   }
   if (e != hipSuccess) return e;
-  if (n_split > 1)
+  if (n_split > 1) {
+    if (a.norm != nullptr && a.kind == LIN_RESID && dtype == 1) {
+      e = launch_split_reduce_norm(a.resid, a.parts, n_split, a.M, a.N, reinterpret_cast<float*>(a.out), *a.norm, s);
+      if (e == hipSuccess && a.norm_done) *a.norm_done = true;
+      if (e != hipErrorNotSupported) return e;
+    }
     return launch_split_reduce(dtype, a.kind == LIN_RESID_F32IN, a.kind == LIN_RESID, a.resid, a.parts, n_split,
                                (size_t)a.M * a.N, a.out, s);
+  }
   return hipSuccess;
 }
 

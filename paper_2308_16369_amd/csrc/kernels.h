@@ -42,6 +42,15 @@ struct RopeArgs {
 };
 hipError_t launch_rope_append(int dtype, const RopeArgs& a, hipStream_t s);
 
+// ---- a norm applied to a linear op's output (rows of N): out = norm(y) * g (+ b).
+struct NormArgs {
+  const void* g;
+  const void* b;        // LayerNorm only
+  void* out;            // [M, N] dtype
+  float eps;
+  bool layer;           // LayerNorm (else RMSNorm)
+};
+
 // ---- linear ops (see sarathi.h for the kinds).
 enum LinearKind { LIN_PLAIN = 0, LIN_RESID = 1, LIN_RESID_F32IN = 2, LIN_SWIGLU = 3, LIN_GELU = 4 };
 struct LinearArgs {
@@ -59,6 +68,12 @@ struct LinearArgs {
   // launch_rope_append).
   const RopeArgs* rope;
   bool* rope_done;
+  // LIN_RESID (bf16), optional: the norm of the output rows folded into the
+  // split-K reduction pass when the op runs split over K (then *norm_done =
+  // true and norm->out holds the normalised rows; else the caller runs the
+  // norm).
+  const NormArgs* norm;
+  bool* norm_done;
 };
 constexpr int MAX_SPLIT = 6;   // split-K partials: at most MAX_SPLIT x [M, N] fp32
 // force_tile >= 0 (bf16, K a multiple of 64): run that producer/consumer tile
@@ -116,5 +131,10 @@ hipError_t launch_attn_combine(int dtype, const CombineArgs& a, hipStream_t s);
 // (resid: fp32 if resid_f32 else dtype; out: fp32 if out_f32 else dtype).
 hipError_t launch_split_reduce(int dtype, bool resid_f32, bool out_f32, const void* resid, const float* parts,
                                int n_split, size_t n, void* out, hipStream_t s);
+// The same for rows x N (bf16 residual, fp32 out) plus the norm of each
+// output row in the same pass (one block per row).  Returns
+// hipErrorNotSupported (nothing launched) when N does not fit one block.
+hipError_t launch_split_reduce_norm(const void* resid, const float* parts, int n_split, int rows, int N, float* out,
+                                    const NormArgs& norm, hipStream_t s);
 
 }  // namespace sarathi

@@ -439,18 +439,24 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
   e = launch_attn_combine(dt, ca, c.s);
   if (e != hipSuccess) return hip_fail(e, "attention combine");
 
-  // postproj + residual -> hres (fp32)
+  // postproj + residual -> hres (fp32), with norm_2 folded into its split-K
+  // reduction pass when it runs split over K
   SARATHI_MARK();
+  NormArgs n2{w->norm2_g, w->norm2_b, ws + c.L.a, cfg->eps, ln};
+  bool norm2_done = false;
   LinearArgs po{};
   po.kind = LIN_RESID; po.M = T; po.N = H; po.K = QD; po.x = ws + c.L.o; po.w = w->w_o; po.resid = x_in;
   po.out = hres; po.parts = parts; po.parts_cap = parts_cap;
+  po.norm = &n2; po.norm_done = &norm2_done;
   e = launch_linear(dt, po, c.s);
   if (e != hipSuccess) return hip_fail(e, "postproj");
 
-  // norm_2
+  // norm_2 (unless folded above)
   SARATHI_MARK();
-  e = launch_norm(dt, true, ln, hres, w->norm2_g, w->norm2_b, ws + c.L.a, T, H, cfg->eps, c.s);
-  if (e != hipSuccess) return hip_fail(e, "norm_2");
+  if (!norm2_done) {
+    e = launch_norm(dt, true, ln, hres, w->norm2_g, w->norm2_b, ws + c.L.a, T, H, cfg->eps, c.s);
+    if (e != hipSuccess) return hip_fail(e, "norm_2");
+  }
 
   // ffn_ln1 + activation
   SARATHI_MARK();
