@@ -108,6 +108,24 @@ def bench_stack(steps: int, warmup: int):
     return out
 
 
+def chunk_key_ranges(offset, C, nh, qblock=128, tau_min=4):
+    """Key ranges per 128-row query block of a chunk, as the runtime plans
+    them: tiles of 64 keys cut into ranges of at most tau tiles, tau chosen
+    to minimise rounds of 512 blocks x (longest range + 4)."""
+    if C <= 0:
+        return []
+    qt = [-(-(offset + min((qb + 1) * qblock, C)) // 64) for qb in range(-(-C // qblock))]
+    best, tau, cand = float("inf"), tau_min, tau_min
+    while cand <= max(max(qt), tau_min):
+        ns = [-(-t // cand) for t in qt]
+        longest = max(-(-t // n) for t, n in zip(qt, ns))
+        cost = -(-(sum(ns) * nh) // 512) * (longest + 4)
+        if cost <= best:
+            best, tau = cost, cand
+        cand += max(1, cand // 4)
+    return [-(-t // tau) for t in qt]
+
+
 def stage_work(shp, b, S_stats=None):
     """Algorithmic FLOPs and HBM bytes of each stage of one layer call.
 
@@ -128,10 +146,10 @@ def stage_work(shp, b, S_stats=None):
     w["preproj"] = (2.0 * T * H * 3 * QD, 3 * QD * H * es + T * H * es + T * 3 * QD * es)
     w["rope_kv_append"] = (0.0, 2 * T * 3 * QD * es + T * QD * es)
     # key-split partials (hd + 2 fp32 per head): decode rows split every 256
-    # keys; chunk rows in 64-row query blocks split every 256 keys (the
-    # runtime's work decomposition)
+    # keys; chunk rows in 128-row query blocks, each block's 64-key tiles cut
+    # into near-equal ranges (the runtime's work decomposition)
     dec_parts = sum(-(-(c + 1) // 256) for c in ctx)
-    pre_parts = sum(64 * -(-(b.chunk_offset + min((qb + 1) * 64, C)) // 256) for qb in range(-(-C // 64)))
+    pre_parts = sum(128 * n for n in chunk_key_ranges(b.chunk_offset, C, nh))
     part_bytes = nh * (hd + 2) * 4
     w["chunk_attention"] = (4.0 * pre_pairs * hd * nh, pre_keys * 2 * QD * es + C * QD * es + pre_parts * part_bytes)
     w["decode_attention"] = (4.0 * dec_keys * hd * nh, dec_keys * 2 * QD * es + B * QD * es + dec_parts * part_bytes)

@@ -5,7 +5,7 @@
 // Chunked-prefill attention (bf16, MFMA): the chunk's queries at positions
 // off..off+C-1 attend to the prefill slot's keys 0..position (the earlier
 // chunks' cached keys plus, causally, the chunk's own; Sec. 4.2).  Work item
-// = (block of PREFILL_QBLOCK queries, split of split_keys keys), one head per
+// = (block of PREFILL_QBLOCK queries, a range of 64-key tiles), one head per
 // block of PREFILL_QBLOCK / 16 waves x 16 query rows.  K and V tiles of 64
 // keys are staged in a ring of LDS stages by LDS DMA (V read back transposed
 // so P*V takes 16 contiguous bytes per lane); S = Q K^T and O += P V run on
@@ -68,10 +68,10 @@ __global__ __launch_bounds__(64 * NW, 4) void attn_prefill_bf16_kernel(PrefillAr
   const int t = (blockIdx.x % 8) * per + blockIdx.x / 8;
   if (t >= a.n_work * a.nh) return;
   const int item = t % a.n_work, h = t / a.n_work;
-  const int* wk = a.work + 3 * item;
+  const int* wk = a.work + 4 * item;
   const int* ch = a.chunks + 4 * wk[0];
   const int slot = ch[0], offset = ch[1], C = ch[2], row0 = ch[3];
-  const int q0 = (wk[1] >> 12) * QB, ksplit = wk[1] & 4095, pslot = wk[2];
+  const int q0 = wk[1] * QB, pslot = wk[2];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int grp = lane >> 4, ql = lane & 15;
   const bf16* qkv = reinterpret_cast<const bf16*>(a.qkv) + (size_t)row0 * a.ld_qkv;
@@ -79,10 +79,10 @@ __global__ __launch_bounds__(64 * NW, 4) void attn_prefill_bf16_kernel(PrefillAr
   const bf16* kbase = cache + (size_t)slot * a.st.slot + (size_t)h * a.st.head;
   const bf16* vbase = kbase + a.st.kv;
 
-  // This item's keys: [kbeg, kend) within 0 .. off + min(q0 + QB, C) - 1.
+  // This item's keys: tiles [t0, t1) of 0 .. off + min(q0 + QB, C) - 1.
   const int n_keys = offset + min(q0 + QB, C);
-  const int kbeg = ksplit * a.split_keys;
-  const int kend = min(n_keys, kbeg + a.split_keys);
+  const int kbeg = (wk[3] >> 16) * KT;
+  const int kend = min(n_keys, (wk[3] & 0xffff) * KT);
   const int n_tiles = (kend - kbeg + KT - 1) / KT;
 
   // The lane's query (B operand of S^T): q = ql, d = ks*32 + 8*grp.

@@ -95,8 +95,8 @@ struct PrefillArgs {
   KVStrides st;
   const int* chunks;    // [n_chunks][slot, offset, len, first row]
   int nh, hd;
-  const int* work;      // [n_work][chunk, (q_block << 12) | key_split, partial slot p]
-  int n_work, split_keys;
+  const int* work;      // [n_work][chunk, q_block, partial slot p, (first key tile << 16) | end key tile]
+  int n_work;
   float* part;          // row j of an item's q-block -> partial index p * PREFILL_QBLOCK + j
 };
 hipError_t launch_attn_prefill(int dtype, const PrefillArgs& a, hipStream_t s);

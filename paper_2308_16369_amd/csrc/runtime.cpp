@@ -104,11 +104,12 @@ Layout make_layout(const sarathi_model_cfg* c, int T, int n_chunks, int S) {
   L.hres = take(T * H * 4);
   L.m = take(T * F * es);
   L.parts = take((size_t)MAX_SPLIT * std::min(T, PARTS_ROWS) * H * 4);
-  // query blocks of 64 rows: each chunk starts a new block
+  // query blocks of QBLOCK rows (each chunk starts a new block), at most one
+  // key range per PRE_SPLIT keys each
   const size_t max_pre = ((size_t)(T + QBLOCK - 1) / QBLOCK + n_chunks - 1) * ((S + PRE_SPLIT - 1) / PRE_SPLIT);
   const size_t max_dec = (size_t)T * ((S + SPLIT_KEYS - 1) / SPLIT_KEYS);
   L.part = take((max_pre * QBLOCK + max_dec) * c->n_heads * (c->head_dim + 2) * 4);
-  L.meta = take(((size_t)T * 5 + (size_t)n_chunks * 4 + max_pre * 3 + max_dec) * 4);
+  L.meta = take(((size_t)T * 5 + (size_t)n_chunks * 4 + max_pre * 4 + max_dec) * 4);
   L.ping0 = take(T * H * es);
   L.ping1 = take(T * H * es);
   L.total = off;
@@ -163,9 +164,9 @@ int from_mixed(const sarathi_mixed_batch* b, BatchDesc* out) {
 
 // Host-side description of the batch and its device metadata.
 struct Plan {
-  int C, B, T, row_base, n_pre, n_dec, n_chunks, pre_split;
+  int C, B, T, row_base, n_pre, n_dec, n_chunks, pre_tiles;
   // row_slot[T] row_pos[T] comb[3T] chunk table [n_chunks][slot, offset, len, first row]
-  // pre_work[n_pre][chunk, (q_block << 12) | key_split, partial slot] dec_work[n_dec]
+  // pre_work[n_pre][chunk, q_block, partial slot, (first tile << 16) | end tile] dec_work[n_dec]
   std::vector<int> meta;
   size_t o_slot, o_pos, o_comb, o_chunks, o_pre, o_dec;   // int offsets into meta
 };
@@ -213,7 +214,7 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
   // item = row x key split).  fp32: every row goes to row attention (a chunk
   // row at position p is attention over keys 0..p, like a decode with ctx = p).
   p.row_base = (cfg->dtype == SARATHI_BF16) ? p.C : 0;
-  p.pre_split = PRE_SPLIT;
+  p.pre_tiles = PRE_SPLIT / 64;
   std::vector<int> slot(p.T), pos(p.T), comb(3 * p.T), tab, pre, dec;
   int r0 = 0;
   for (const ChunkDesc& c : b.chunks) {
@@ -227,29 +228,48 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
     // QBLOCK partial rows apart); the work items run split by split so that
     // the query blocks that read the same keys are neighbours (and share an
     // XCD's L2, see the chunk-attention kernel).
-    // Key split: the largest (PRE_SPLIT x 2^j) that still fills both block
-    // slots of every CU (two blocks run per CU; fewer, longer items write
-    // fewer partials); PRE_SPLIT when even that leaves slots idle.
-    auto n_blocks = [&](int split) {
-      long n = 0;
-      for (const ChunkDesc& c : b.chunks)
-        for (int qb = 0; qb * QBLOCK < c.len; ++qb)
-          n += (c.offset + std::min((qb + 1) * QBLOCK, c.len) + split - 1) / split;
-      return n * cfg->n_heads;
-    };
-    p.pre_split = PRE_SPLIT;
-    while (p.pre_split < (1 << 20) && n_blocks(2 * p.pre_split) >= 512) p.pre_split *= 2;
-    const int split = p.pre_split;
+    // Key ranges: each q-block's keys, in 64-key tiles, are cut into ns
+    // near-equal ranges of at most tau tiles (tau >= PRE_SPLIT / 64).  tau
+    // minimises rounds of blocks (two per CU) x (largest range + ~4 tiles of
+    // fixed cost per block), fitted to measurements of the LLaMA-33B and
+    // GPT-3 chunk shapes; ties go to the larger tau (fewer partials).
+    std::vector<int> qtiles;   // tiles of every q-block, chunk by chunk
+    int t_max = 1;
+    for (const ChunkDesc& c : b.chunks)
+      for (int qb = 0; qb * QBLOCK < c.len; ++qb) {
+        const int n_keys = c.offset + std::min((qb + 1) * QBLOCK, c.len);
+        qtiles.push_back((n_keys + 63) / 64);
+        t_max = std::max(t_max, qtiles.back());
+      }
+    const int tau_min = PRE_SPLIT / 64;
+    int tau = tau_min;
+    double best = 1e300;
+    for (int cand = tau_min; cand <= std::max(t_max, tau_min); cand += std::max(1, cand / 4)) {
+      long blocks = 0;
+      int longest = 0;
+      for (int t : qtiles) {
+        const int ns = (t + cand - 1) / cand;
+        blocks += ns;
+        longest = std::max(longest, (t + ns - 1) / ns);
+      }
+      blocks *= cfg->n_heads;
+      const double cost = (double)((blocks + 511) / 512) * (longest + 4);
+      if (cost <= best) {
+        best = cost;
+        tau = cand;
+      }
+    }
+    p.pre_tiles = tau;
     r0 = 0;
-    int slot_base = 0;
+    int slot_base = 0, qi = 0;
     for (int ci = 0; ci < p.n_chunks; ++ci) {
       const ChunkDesc& c = b.chunks[ci];
       const int nqb = (c.len + QBLOCK - 1) / QBLOCK;
-      std::vector<int> ns(nqb), first(nqb);
+      std::vector<int> ns(nqb), first(nqb), nt(nqb);
       int max_ns = 0;
       for (int qb = 0; qb < nqb; ++qb) {
-        const int n_keys = c.offset + std::min((qb + 1) * QBLOCK, c.len);
-        ns[qb] = (n_keys + split - 1) / split;
+        nt[qb] = qtiles[qi++];
+        ns[qb] = (nt[qb] + tau - 1) / tau;
         first[qb] = slot_base;
         slot_base += ns[qb];
         max_ns = std::max(max_ns, ns[qb]);
@@ -261,11 +281,14 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
       }
       for (int s = 0; s < max_ns; ++s)
         for (int qb = 0; qb < nqb; ++qb)
-          if (s < ns[qb]) pre.insert(pre.end(), {ci, (qb << 12) | s, first[qb] + s});
+          if (s < ns[qb]) {
+            const int t0 = (int)((long)nt[qb] * s / ns[qb]), t1 = (int)((long)nt[qb] * (s + 1) / ns[qb]);
+            pre.insert(pre.end(), {ci, qb, first[qb] + s, (t0 << 16) | t1});
+          }
       r0 += c.len;
     }
   }
-  const int pre_rows = (int)pre.size() / 3 * QBLOCK;
+  const int pre_rows = (int)pre.size() / 4 * QBLOCK;
   // Row-attention items run in the order of the rows' KV slots (each row's
   // splits together), so the blocks in flight stream the cache in address
   // order (measured ~2% faster than a random slot order).
@@ -279,7 +302,7 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
     comb[3 * r + 2] = 1;
     for (int s = 0; s < ns; ++s) dec.push_back(((r - p.row_base) << 12) | s);
   }
-  p.n_pre = (int)pre.size() / 3;
+  p.n_pre = (int)pre.size() / 4;
   p.n_dec = (int)dec.size();
   p.meta.reserve(5 * p.T + tab.size() + pre.size() + dec.size());
   p.o_slot = 0; p.meta.insert(p.meta.end(), slot.begin(), slot.end());
@@ -418,7 +441,7 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
     PrefillArgs pa{};
     pa.qkv = ws + c.L.qkv; pa.ld_qkv = 3 * QD; pa.kv_layer = kv_layer; pa.st = c.kv->st;
     pa.chunks = meta + P.o_chunks; pa.nh = nh; pa.hd = hd;
-    pa.work = meta + P.o_pre; pa.n_work = P.n_pre; pa.split_keys = P.pre_split; pa.part = part;
+    pa.work = meta + P.o_pre; pa.n_work = P.n_pre; pa.part = part;
     e = launch_attn_prefill(dt, pa, c.s);
     if (e != hipSuccess) return hip_fail(e, "chunk attention");
   }
