@@ -6,10 +6,12 @@
 // Row attention (decodes; in fp32 runs also the chunk rows): each row attends
 // to keys 0..pos of its slot.  Work item = (row, split of split_keys keys); a
 // block of 4 waves streams its split, each wave 32 keys per pass with 16-byte
-// loads (a key row spread over hd*size/16 lanes), partial dot products
-// reduce-scattered across those lanes so each key's score ends up in two
-// lanes, wave-level online softmax, then P*V accumulated per lane.  The
-// block's four wave states are merged in LDS into one partial.
+// non-temporal loads (a key row spread over hd*size/16 lanes), partial dot
+// products reduce-scattered across those lanes so each key's score ends up in
+// two lanes, online softmax, then P*V accumulated per lane.  The block's four
+// wave states are merged in LDS into one partial.  attn_rows_kernel is the
+// generic form (fp32 runs); attn_rows_bf16_kernel the bf16 one, with the
+// arithmetic arranged for fewer vector-ALU instructions (see there).
 #include "kernels.h"
 
 namespace sarathi {
