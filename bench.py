@@ -145,10 +145,10 @@ def stage_work(shp, b, S_stats=None):
     w["norm_1"] = (0.0, 2 * T * H * es + T * H * 4)
     w["preproj"] = (2.0 * T * H * 3 * QD, 3 * QD * H * es + T * H * es + T * 3 * QD * es)
     w["rope_kv_append"] = (0.0, 2 * T * 3 * QD * es + T * QD * es)
-    # key-split partials (hd + 2 fp32 per head): decode rows split every 256
+    # key-split partials (hd + 2 fp32 per head): decode rows split every 512
     # keys; chunk rows in 128-row query blocks, each block's 64-key tiles cut
     # into near-equal ranges (the runtime's work decomposition)
-    dec_parts = sum(-(-(c + 1) // 256) for c in ctx)
+    dec_parts = sum(-(-(c + 1) // 512) for c in ctx)
     pre_parts = sum(128 * n for n in chunk_key_ranges(b.chunk_offset, C, nh))
     part_bytes = nh * (hd + 2) * 4
     w["chunk_attention"] = (4.0 * pre_pairs * hd * nh, pre_keys * 2 * QD * es + C * QD * es + pre_parts * part_bytes)

@@ -48,7 +48,7 @@ int hip_fail(hipError_t e, const char* what) {
   return fail(SARATHI_EHIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-constexpr int SPLIT_KEYS = 256;   // keys per decode-attention work item
+constexpr int SPLIT_KEYS = 512;   // keys per decode-attention work item
 constexpr int PRE_SPLIT = 256;    // smallest key split of a chunk-attention work item
 constexpr int QBLOCK = PREFILL_QBLOCK;   // chunk rows per chunk-attention work item
 constexpr int PARTS_ROWS = 512;   // split-K partials are sized for batches up to this many rows (larger
