@@ -5,11 +5,11 @@
 //
 // Row attention (decodes; in fp32 runs also the chunk rows): each row attends
 // to keys 0..pos of its slot.  Work item = (row, split of split_keys keys); a
-// block of 4 waves streams its split, each wave 32 keys per pass with 16-byte
-// non-temporal loads (a key row spread over hd*size/16 lanes), partial dot
-// products reduce-scattered across those lanes so each key's score ends up in
-// two lanes, online softmax, then P*V accumulated per lane.  The block's four
-// wave states are merged in LDS into one partial.  attn_rows_kernel is the
+// block of 4 (fp32) or 8 (bf16) waves streams its split, each wave 32 keys per
+// pass with 16-byte non-temporal loads (a key row spread over hd*size/16
+// lanes), partial dot products reduce-scattered across those lanes so each
+// key's score ends up in two lanes, online softmax, then P*V accumulated per
+// lane.  The block's wave states are merged in LDS into one partial.  attn_rows_kernel is the
 // generic form (fp32 runs); attn_rows_bf16_kernel the bf16 one, with the
 // arithmetic arranged for fewer vector-ALU instructions (see there).
 #include "kernels.h"
@@ -241,16 +241,16 @@ __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
 //   key's probability reaches the group's lanes by a row broadcast; the
 //   groups are merged once at the end;
 //   P V stays fp32 (probabilities and V unpacked to fp32).
-template <int D>
-__global__ __launch_bounds__(256) void attn_rows_bf16_kernel(RowAttnArgs a, float scale_log2) {
+template <int D, int NWV>
+__global__ __launch_bounds__(64 * NWV) void attn_rows_bf16_kernel(RowAttnArgs a, float scale_log2) {
   constexpr int LPK = D / 8;                 // lanes per key row (8 bf16 per lane)
   constexpr int KPI = 64 / LPK;              // keys per wave load instruction
   constexpr int DUP = 2;                     // lanes holding each key's score
   constexpr int NI = LPK / DUP;              // load instructions per pass (K, and V)
   constexpr int KP = NI * KPI;               // keys per pass per wave
   static_assert(LPK == 16 || LPK == 8, "head_dim 128 or 64");
-  __shared__ float red_m[4], red_l[4];
-  __shared__ float red_o[4][D];
+  __shared__ float red_m[NWV], red_l[NWV];
+  __shared__ float red_o[NWV][D];
 
   const int item = blockIdx.x, h = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -275,10 +275,10 @@ __global__ __launch_bounds__(256) void attn_rows_bf16_kernel(RowAttnArgs a, floa
 #pragma unroll
   for (int e = 0; e < 8; ++e) o[e] = 0.f;
 
-  // Passes of KP keys per wave (pb, pb + 4*KP, ...): all K loads, then all V
+  // Passes of KP keys per wave (pb, pb + NWV*KP, ...): all K loads, then all V
   // loads, non-temporal (see attn_rows_kernel); addresses past the split are
   // clamped to its last key (finite data, masked below).
-  for (int pb = kb + wave * KP; pb < ke; pb += 4 * KP) {
+  for (int pb = kb + wave * KP; pb < ke; pb += NWV * KP) {
     uint4 kr[NI], vr[NI];
     // element offsets in 32 bits: positions < 2^20, position stride = head_dim
     uint32_t off[NI];
@@ -347,19 +347,21 @@ __global__ __launch_bounds__(256) void attn_rows_bf16_kernel(RowAttnArgs a, floa
     for (int e = 0; e < 8; ++e) red_o[wave][j * 8 + e] = o[e];
   }
   __syncthreads();
-  const float Mb = fmaxf(fmaxf(red_m[0], red_m[1]), fmaxf(red_m[2], red_m[3]));
+  float Mb = red_m[0];
+#pragma unroll
+  for (int w = 1; w < NWV; ++w) Mb = fmaxf(Mb, red_m[w]);
   const float Ms = (Mb == -INFINITY) ? 0.f : Mb;
   float* dst = a.part + ((size_t)(a.part_base + item) * a.nh + h) * (D + 2);
-  for (int d = tid; d < D; d += 256) {
+  for (int d = tid; d < D; d += 64 * NWV) {
     float acc = 0.f;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) acc += red_o[w][d] * exp2f(red_m[w] - Ms);
+    for (int w = 0; w < NWV; ++w) acc += red_o[w][d] * exp2f(red_m[w] - Ms);
     dst[2 + d] = acc;
   }
   if (tid == 0) {
     float Lb = 0.f;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) Lb += red_l[w] * exp2f(red_m[w] - Ms);
+    for (int w = 0; w < NWV; ++w) Lb += red_l[w] * exp2f(red_m[w] - Ms);
     dst[0] = Mb;
     dst[1] = Lb;
   }
@@ -376,10 +378,11 @@ hipError_t launch_attn_rows(int dtype, const RowAttnArgs& a, hipStream_t s) {
   if (a.n_work <= 0) return hipSuccess;
   if (dtype == 0) return a.hd == 128 ? run_rows<float, 128>(a, s) : run_rows<float, 64>(a, s);
   const float scale_log2 = LOG2E / sqrtf((float)a.hd);
+  constexpr int NWV = 8;
   if (a.hd == 128)
-    hipLaunchKernelGGL((attn_rows_bf16_kernel<128>), dim3(a.n_work, a.nh), dim3(256), 0, s, a, scale_log2);
+    hipLaunchKernelGGL((attn_rows_bf16_kernel<128, NWV>), dim3(a.n_work, a.nh), dim3(64 * NWV), 0, s, a, scale_log2);
   else
-    hipLaunchKernelGGL((attn_rows_bf16_kernel<64>), dim3(a.n_work, a.nh), dim3(256), 0, s, a, scale_log2);
+    hipLaunchKernelGGL((attn_rows_bf16_kernel<64, NWV>), dim3(a.n_work, a.nh), dim3(64 * NWV), 0, s, a, scale_log2);
   return hipGetLastError();
 }
 
