@@ -531,6 +531,11 @@ int prepare(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, int n_
   if (overlap(xi, xbytes, wb, L->total) || overlap(xo, xbytes, wb, L->total) || overlap(xi, xbytes, xo, xbytes))
     return fail(SARATHI_EINVAL, "x_in, x_out and the workspace must not overlap");
   *plan = make_plan(cfg, batch);
+  // the plan must fit the regions the layout sized for it (an internal
+  // invariant: the bounds above hold for every batch check_batch accepts)
+  const size_t part_rows = (L->meta - L->part) / ((size_t)cfg->n_heads * (cfg->head_dim + 2) * 4);
+  if (plan->meta.size() * 4 > L->ping0 - L->meta || (size_t)plan->n_pre * QBLOCK + plan->n_dec > part_rows)
+    return fail(SARATHI_EINVAL, "internal: batch plan exceeds its workspace layout");
   return SARATHI_OK;
 }
 
