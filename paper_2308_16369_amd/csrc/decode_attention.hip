@@ -252,7 +252,10 @@ __global__ __launch_bounds__(64 * NWV) void attn_rows_bf16_kernel(RowAttnArgs a,
   __shared__ float red_m[NWV], red_l[NWV];
   __shared__ float red_o[NWV][D];
 
-  const int item = blockIdx.x, h = blockIdx.y;
+  // one block per (work item, head), heads fastest: the blocks in flight
+  // stream the same key range of one slot for all its heads (measured ~2%
+  // faster than items fastest)
+  const int item = blockIdx.x / a.nh, h = blockIdx.x % a.nh;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane / LPK, j = lane % LPK;
   const int wv = a.work[item];
@@ -379,10 +382,11 @@ hipError_t launch_attn_rows(int dtype, const RowAttnArgs& a, hipStream_t s) {
   if (dtype == 0) return a.hd == 128 ? run_rows<float, 128>(a, s) : run_rows<float, 64>(a, s);
   const float scale_log2 = LOG2E / sqrtf((float)a.hd);
   constexpr int NWV = 8;
+  const unsigned grid = (unsigned)((size_t)a.n_work * a.nh);
   if (a.hd == 128)
-    hipLaunchKernelGGL((attn_rows_bf16_kernel<128, NWV>), dim3(a.n_work, a.nh), dim3(64 * NWV), 0, s, a, scale_log2);
+    hipLaunchKernelGGL((attn_rows_bf16_kernel<128, NWV>), dim3(grid), dim3(64 * NWV), 0, s, a, scale_log2);
   else
-    hipLaunchKernelGGL((attn_rows_bf16_kernel<64, NWV>), dim3(a.n_work, a.nh), dim3(64 * NWV), 0, s, a, scale_log2);
+    hipLaunchKernelGGL((attn_rows_bf16_kernel<64, NWV>), dim3(grid), dim3(64 * NWV), 0, s, a, scale_log2);
   return hipGetLastError();
 }
 
