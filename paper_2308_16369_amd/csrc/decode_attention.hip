@@ -180,15 +180,23 @@ __device__ __forceinline__ float row_bcast_c(float v) {
   return __builtin_amdgcn_update_dpp(0.f, v, 0x150 + L, 0xf, 0xf, false);
 }
 __device__ __forceinline__ float row_bcast(float v, int l) {
-  switch (l) {
+  switch (l & 15) {
     case 0: return row_bcast_c<0>(v);
+    case 1: return row_bcast_c<1>(v);
     case 2: return row_bcast_c<2>(v);
+    case 3: return row_bcast_c<3>(v);
     case 4: return row_bcast_c<4>(v);
+    case 5: return row_bcast_c<5>(v);
     case 6: return row_bcast_c<6>(v);
+    case 7: return row_bcast_c<7>(v);
     case 8: return row_bcast_c<8>(v);
+    case 9: return row_bcast_c<9>(v);
     case 10: return row_bcast_c<10>(v);
+    case 11: return row_bcast_c<11>(v);
     case 12: return row_bcast_c<12>(v);
-    default: return row_bcast_c<14>(v);
+    case 13: return row_bcast_c<13>(v);
+    case 14: return row_bcast_c<14>(v);
+    default: return row_bcast_c<15>(v);
   }
 }
 template <int LPK>
