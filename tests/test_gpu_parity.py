@@ -276,6 +276,49 @@ def test_mixed_batch_layer(dtype, case):
     run_mixed_and_check(wl.make_instance(shape, b, max_seq_len=S_, n_slots=ns, seed=17), f"mixed {case} {dtype}")
 
 
+def _random_batch(rng, S_, n_slots, mixed):
+    """A random batch over distinct slots: 0-3 prompt chunks (at most one for
+    the hybrid entry point) at random offsets and lengths, 0-79 decodes at
+    random context lengths, at least one row."""
+    slots = rng.permutation(n_slots)
+    k = int(rng.integers(0, 4)) if mixed else int(rng.integers(0, 2))
+    chunks = []
+    for i in range(k):
+        n = int(rng.choice([1, int(rng.integers(2, 130)), int(rng.integers(130, 400))]))
+        off = int(rng.integers(0, S_ - n + 1))
+        chunks.append((int(slots[i]), off, n))
+    B = int(rng.integers(0 if k else 1, 80))
+    ctx = rng.integers(0, S_, size=B)
+    ctx[: B // 4] = rng.choice([0, 511, 512, 1023, S_ - 1], size=B // 4)   # split boundaries and the ends
+    ds = np.array(slots[k:k + B], np.int32)
+    if mixed:
+        return wl.MixedBatch(chunks=chunks, decode_slots=ds, decode_ctx=np.array(ctx, np.int32))
+    ps, off, C = chunks[0] if chunks else (-1, 0, 0)
+    return wl.Batch(prefill_slot=ps, chunk_offset=off, chunk_len=C, decode_slots=ds,
+                    decode_ctx=np.array(ctx, np.int32))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("seed", range(8))
+def test_random_batches(dtype, seed):
+    """Seeded random batches through both entry points (hybrid: one chunk or
+    none; mixed: up to three), head_dim 64 and 128, a cache of 1100
+    positions so decodes cross 512-key splits and chunks span many key
+    tiles; every output, intermediate and KV entry against the oracle."""
+    rng = np.random.default_rng(1000 + seed)
+    mixed = seed % 2 == 1
+    hd128 = seed % 3 != 0
+    shape = _tiny_shape(dtype, hidden=512, n_heads=4, head_dim=128, ffn=1376) if hd128 else _tiny_shape(dtype)
+    S_, ns = 1100, 84
+    b = _random_batch(rng, S_, ns, mixed)
+    inst = wl.make_instance(shape, b, max_seq_len=S_, n_slots=ns, seed=2000 + seed)
+    label = f"random {'mixed' if mixed else 'hybrid'} seed {seed} hd {shape.head_dim} {dtype}"
+    if mixed:
+        run_mixed_and_check(inst, label)
+    else:
+        run_and_check(inst, label)
+
+
 def test_mixed_model_step_three_layers_bf16():
     shape = dataclasses.replace(_tiny_shape("bf16"), n_layers=3)
     chunks, decs, S_, ns = MIXED["three_chunks_and_decodes"]
