@@ -108,6 +108,22 @@ def bench_stack(steps: int, warmup: int):
     return out
 
 
+def per_call_ms(make_call, stream, steps):
+    """Time of each of ``steps`` consecutive calls, from HIP events recorded
+    between them on the launch stream (one event per call boundary)."""
+    import torch
+    call, keep = make_call()
+    call()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    ev[0].record(stream)
+    for i in range(steps):
+        call()
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    return [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+
+
 def chunk_key_ranges(offset, C, nh, qblock=128, tau_min=4):
     """Key ranges per 128-row query block of a chunk, as the runtime plans
     them: tiles of 64 keys cut into ranges of at most tau tiles, tau chosen
@@ -253,11 +269,19 @@ def main():
             stages = {k: v / n for k, v in stages.items()}
         return e0.elapsed_time(e1) / steps, wall / steps * 1e3, stages
 
+    def run_once(batch, xin, xout):
+        bb, keep = S.make_batch(batch.prefill_slot, batch.chunk_offset, batch.chunk_len,
+                                list(batch.decode_slots), list(batch.decode_ctx))
+        return lambda: S.sarathi_hybrid_layer_forward(cfg, wabi, kv, 0, bb, xin.data_ptr(), xout.data_ptr(),
+                                                      ws.data_ptr(), ws_bytes, stream.cuda_stream), keep
+
     # ---- timed region: K hybrid steps, with per-stage HIP events on the launch stream
     ms, wall_ms, stages = run(b, x, y, args.steps, args.warmup, profile=True)
     # ---- same steps without the stage events (the events' own cost)
     ms_plain, _, _ = run(b, x, y, args.steps, 2)
     print(f"# hybrid: {ms:.4f} ms/step with stage events, {ms_plain:.4f} without", file=sys.stderr, flush=True)
+    # ---- spread: the same steps with one event between consecutive calls
+    per_call = per_call_ms(lambda: run_once(b, x, y), stream, args.steps)
 
     # ---- decode accounting (Sec. 5.1.1): prefill-only and decode-only batches of the same rows
     extra = {}
@@ -309,6 +333,8 @@ def main():
                 "frac": dk["hbm_frac"]}
     roof["kernel"] = dom
     roof["traffic"] = counter_traffic(dom, w.name)
+    # layer roofline: every stage at the larger of its MFMA and HBM times
+    roof_ms = sum(max(fl / (peak_flops * 1e12), by / (PEAK_HBM_GBPS * 1e9)) for fl, by in work.values()) * 1e3
     lin = ["preproj", "postproj", "ffn_ln1", "ffn_ln2"]
     lin_ms = sum(kernels[k]["ms"] for k in lin if k in kernels)
     lin_flops = sum(work[k][0] for k in lin)
@@ -362,6 +388,8 @@ def main():
                    "ctx_range": [w.batch.ctx_lo, w.batch.ctx_hi], "rows": T, "parallelism": "none (1 GPU)"},
         "roofline": roof,
         "cpu_baseline": cpu,
+        "layer_roofline": {"ms": round(roof_ms, 5), "frac": round(roof_ms / ms_plain, 4)},
+        "ms_per_call_p10_p50_p90": [round(float(np.percentile(per_call, q)), 5) for q in (10, 50, 90)],
         "ms_per_step_with_stage_events": round(ms, 5),
         "wall_ms_per_step": round(wall_ms, 5),
         "linear_ops": {"ms": round(lin_ms, 5), "mfma_frac": round(lin_flops / (lin_ms * 1e-3) / 1e12 / peak_flops, 4),
