@@ -470,11 +470,12 @@ __global__ __launch_bounds__(64 * (WGM * WGN + NP)) void gemm_ws_kernel(GemmP p)
 }
 
 // ============================================================================ fp32 FMA
-// 64x64 tile of W rows (SwiGLU: 32 gate + 32 up rows -> 32 outputs), BK 16,
+// 64x64 tile of W rows (SwiGLU: 32 gate + 32 up rows -> 32 outputs), BK 64
+// (few k-steps: the small fp32 matmuls run few blocks and are latency-bound),
 // 16x16 threads with 4x4 results each.
 template <int EPI>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmP p) {
-  constexpr int BK = 16;
+  constexpr int BK = 64;
   __shared__ float As[BK][64 + 4];
   __shared__ float Ws[BK][64 + 4];
   const int tile_m = blockIdx.x, tile_n = blockIdx.y;
@@ -487,22 +488,39 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmP p) {
 #pragma unroll
   for (int j = 0; j < 4; ++j) cols[j] = (EPI == EPI_SWIGLU) ? ((j < 2) ? 2 * tx + j : 32 + 2 * tx + j - 2) : 4 * tx + j;
   float acc[4][4] = {};
+  // Each thread stages PER elements of A and of W per k-step.  All loads are
+  // issued before any is used (addresses clamped into the operands, values
+  // outside them zeroed afterwards), so a k-step waits for one memory round
+  // trip rather than one per element.
+  constexpr int PER = 64 * BK / 256;
   for (int k0 = 0; k0 < p.K; k0 += BK) {
-    for (int e = threadIdx.x; e < 64 * BK; e += 256) {
+    float ra[PER], rw[PER];
+    bool oka[PER], okw[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = threadIdx.x + i * 256;
       const int r = e / BK, kk = e % BK;
       const int gr = m0 + r, gk = k0 + kk;
-      As[kk][r] = (gr < p.M && gk < p.K) ? A[(size_t)gr * p.K + gk] : 0.f;
-      int wrow;
-      bool ok;
+      const int ck = min(gk, p.K - 1);
+      int wrow, jn;
       if (EPI == EPI_SWIGLU) {
-        const int j = n0_out + (r % 32);
-        ok = j < p.N;
-        wrow = (r < 32) ? j : p.N + j;
+        jn = n0_out + (r % 32);
+        wrow = (r < 32) ? min(jn, p.N - 1) : p.N + min(jn, p.N - 1);
       } else {
-        wrow = n0_out + r;
-        ok = wrow < p.N;
+        jn = n0_out + r;
+        wrow = min(jn, p.N - 1);
       }
-      Ws[kk][r] = (ok && gk < p.K) ? W[(size_t)wrow * p.K + gk] : 0.f;
+      oka[i] = gr < p.M && gk < p.K;
+      okw[i] = jn < p.N && gk < p.K;
+      ra[i] = A[(size_t)min(gr, p.M - 1) * p.K + ck];
+      rw[i] = W[(size_t)wrow * p.K + ck];
+    }
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = threadIdx.x + i * 256;
+      const int r = e / BK, kk = e % BK;
+      As[kk][r] = oka[i] ? ra[i] : 0.f;
+      Ws[kk][r] = okw[i] ? rw[i] : 0.f;
     }
     __syncthreads();
 #pragma unroll
