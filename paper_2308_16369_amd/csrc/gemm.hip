@@ -479,6 +479,9 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmP p) {
   __shared__ float As[BK][64 + 4];
   __shared__ float Ws[BK][64 + 4];
   const int tile_m = blockIdx.x, tile_n = blockIdx.y;
+  // split-K (EPI_PARTIAL): blockIdx.z takes k in [z * k_split, (z + 1) * k_split)
+  const int split = blockIdx.z;
+  const int kbeg = split * p.k_split, kend = min(p.K, kbeg + p.k_split);
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
   const int m0 = tile_m * 64;
   const int n0_out = tile_n * (EPI == EPI_SWIGLU ? 32 : 64);
@@ -493,7 +496,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmP p) {
   // outside them zeroed afterwards), so a k-step waits for one memory round
   // trip rather than one per element.
   constexpr int PER = 64 * BK / 256;
-  for (int k0 = 0; k0 < p.K; k0 += BK) {
+  for (int k0 = kbeg; k0 < kend; k0 += BK) {
     float ra[PER], rw[PER];
     bool oka[PER], okw[PER];
 #pragma unroll
@@ -510,8 +513,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmP p) {
         jn = n0_out + r;
         wrow = min(jn, p.N - 1);
       }
-      oka[i] = gr < p.M && gk < p.K;
-      okw[i] = jn < p.N && gk < p.K;
+      oka[i] = gr < p.M && gk < kend;
+      okw[i] = jn < p.N && gk < kend;
       ra[i] = A[(size_t)min(gr, p.M - 1) * p.K + ck];
       rw[i] = W[(size_t)wrow * p.K + ck];
     }
@@ -552,7 +555,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmP p) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int c = n0_out + 4 * tx + j;
-        if (c < p.N) epi_store<float, EPI>(p, r, c, acc[i][j]);
+        if (c < p.N) epi_store<float, EPI>(p, r, c, acc[i][j], split);
       }
     }
   }
@@ -601,7 +604,7 @@ static hipError_t run_bf16_epi(int epi, const GemmP& p, hipStream_t s) {
 template <int EPI>
 static hipError_t run_f32(const GemmP& p, hipStream_t s) {
   const int out_per_tile = (EPI == EPI_SWIGLU) ? 32 : 64;
-  dim3 grid((p.M + 63) / 64, (p.N + out_per_tile - 1) / out_per_tile);
+  dim3 grid((p.M + 63) / 64, (p.N + out_per_tile - 1) / out_per_tile, p.n_split);
   hipLaunchKernelGGL(gemm_f32_kernel<EPI>, grid, dim3(256), 0, s, p);
   return hipGetLastError();
 }
@@ -725,6 +728,25 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s, int forc
   p.k_split = a.K; p.n_split = 1;
 
   if (dtype == 0) {
+    // Split-K for the residual ops when the 64x64 tiles leave most CUs idle:
+    // fp32 partials per split of whole 64-wide k-steps, then residual +
+    // partials added in split order (deterministic).
+    const bool resid_kind = a.kind == LIN_RESID || a.kind == LIN_RESID_F32IN;
+    const int tiles = ((a.M + 63) / 64) * ((a.N + 63) / 64);
+    if (resid_kind && a.parts != nullptr && tiles < 64) {
+      int ns = std::min(std::min(MAX_SPLIT, (64 + tiles - 1) / tiles), (a.K + 127) / 128);
+      ns = (int)std::min<size_t>((size_t)ns, a.parts_cap / ((size_t)a.M * a.N));
+      if (ns > 1) {
+        const int steps = (a.K + 63) / 64;
+        p.k_split = (steps + ns - 1) / ns * 64;
+        p.n_split = (a.K + p.k_split - 1) / p.k_split;
+        p.out = a.parts;
+        hipError_t e = run_f32<EPI_PARTIAL>(p, s);
+        if (e != hipSuccess) return e;
+        return launch_split_reduce(0, a.kind == LIN_RESID_F32IN, a.kind == LIN_RESID, a.resid, a.parts, p.n_split,
+                                   (size_t)a.M * a.N, a.out, s);
+      }
+    }
     switch (a.kind) {
       case LIN_PLAIN: return run_f32<EPI_STORE>(p, s);
       case LIN_GELU: return run_f32<EPI_GELU>(p, s);
