@@ -241,6 +241,20 @@ def test_layer_long_chunk_bf16(C, off, decodes):
     run_and_check(wl.make_instance(shape, b, max_seq_len=3072, n_slots=3, seed=41), f"long chunk {C}@{off}")
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_layer_long_contexts(dtype):
+    """Contexts of tens of thousands of keys: decodes of 65 and 137 512-key
+    splits (the combine pass reads a row's partials 64 splits at a time, so
+    this crosses one and two of its chunk boundaries) and a 100-row chunk
+    after 50000 cached positions (its query blocks cut ~780 key tiles into
+    ranges)."""
+    S_ = 70016
+    shape = _tiny_shape(dtype, hidden=128, n_heads=2, head_dim=64, ffn=256)
+    b = wl.Batch(prefill_slot=1, chunk_offset=50000, chunk_len=100, decode_slots=np.array([3, 0], np.int32),
+                 decode_ctx=np.array([69999, 33000], np.int32))
+    run_and_check(wl.make_instance(shape, b, max_seq_len=S_, n_slots=4, seed=29), f"long contexts {dtype}")
+
+
 MIXED = {
     # name: (chunks [(slot, offset, len)], decodes [(slot, ctx)], max_seq_len, n_slots)
     "three_chunks_and_decodes": ([(2, 100, 37), (0, 0, 64), (5, 190, 65)], [(1, 77), (3, 0), (7, 250)], 256, 9),
