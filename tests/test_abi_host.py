@@ -80,6 +80,13 @@ def test_kv_alloc_rejects_small_memory_and_nulls(lib):
     assert lib.sarathi_kv_alloc(ct.byref(cfg), 0, 256, ct.c_void_p(FAKE_DEV), need, ct.byref(h)) == S.EINVAL
     assert lib.sarathi_kv_alloc(None, 9, 256, ct.c_void_p(FAKE_DEV), need, ct.byref(h)) == S.EINVAL
     assert lib.sarathi_kv_alloc(ct.byref(cfg), 9, 256, ct.c_void_p(FAKE_DEV + 2), need, ct.byref(h)) == S.EINVAL
+    # the largest accepted cache length (positions < 2^20) and the first rejected one
+    top = S.sarathi_kv_bytes(cfg, 1, 1 << 20)
+    assert lib.sarathi_kv_alloc(ct.byref(cfg), 1, 1 << 20, ct.c_void_p(FAKE_DEV), top, ct.byref(h)) == S.OK
+    lib.sarathi_kv_free(h)
+    assert lib.sarathi_kv_alloc(ct.byref(cfg), 1, (1 << 20) + 1, ct.c_void_p(FAKE_DEV), 2 * top,
+                                ct.byref(h)) == S.EINVAL
+    assert lib.sarathi_kv_alloc(ct.byref(cfg), (1 << 20) + 1, 1, ct.c_void_p(FAKE_DEV), 1 << 40, ct.byref(h)) == S.EINVAL
 
 
 def test_workspace_layout_is_consistent(lib):
