@@ -153,9 +153,13 @@ def round_to_bf16(a: np.ndarray) -> np.ndarray:
     """Round fp32 values to the nearest bf16 (ties to even); returns fp32
     holding exactly representable bf16 values.  NaN stays a quiet NaN."""
     a = np.ascontiguousarray(a, dtype=np.float32)
-    u = a.view(np.uint32).astype(np.uint64)
-    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) << 16
-    out = r.astype(np.uint32).view(np.float32)
+    u = a.view(np.uint32)
+    # 32-bit arithmetic: the sum wraps only for bit patterns above 0xFFFF7FFF,
+    # which are all NaNs (restored below)
+    r = u + ((u >> 16) & np.uint32(1))
+    r += np.uint32(0x7FFF)
+    r &= np.uint32(0xFFFF0000)
+    out = r.view(np.float32)
     nan = np.isnan(a)
     if nan.any():
         out = out.copy()
