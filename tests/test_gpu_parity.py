@@ -255,6 +255,17 @@ def test_layer_long_contexts(dtype):
     run_and_check(wl.make_instance(shape, b, max_seq_len=S_, n_slots=4, seed=29), f"long contexts {dtype}")
 
 
+def test_layer_max_cache_length_bf16():
+    """The longest cache the library accepts (2^20 positions): a decode at
+    the last position (2048 key splits) and an 8-row chunk ending there
+    (16384 key tiles for its query block)."""
+    S_ = 1 << 20
+    shape = _tiny_shape("bf16", hidden=64, n_heads=1, head_dim=64, ffn=128)
+    b = wl.Batch(prefill_slot=1, chunk_offset=S_ - 8, chunk_len=8, decode_slots=np.array([0], np.int32),
+                 decode_ctx=np.array([S_ - 1], np.int32))
+    run_and_check(wl.make_instance(shape, b, max_seq_len=S_, n_slots=2, seed=31), "max cache length bf16")
+
+
 MIXED = {
     # name: (chunks [(slot, offset, len)], decodes [(slot, ctx)], max_seq_len, n_slots)
     "three_chunks_and_decodes": ([(2, 100, 37), (0, 0, 64), (5, 190, 65)], [(1, 77), (3, 0), (7, 250)], 256, 9),
