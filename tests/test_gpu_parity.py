@@ -164,6 +164,35 @@ def test_linear_split_k_deterministic(kind):
         assert err <= TOL["bf16"]
 
 
+@pytest.mark.parametrize("kind", [S.LINEAR_RESID, S.LINEAR_RESID_F32IN])
+@pytest.mark.parametrize("mnk", [(72, 256, 688), (5, 17, 1000), (130, 200, 4104)])
+def test_linear_split_k_fp32(kind, mnk):
+    """fp32 residual ops split over K when their 64x64 tiles leave most CUs
+    idle (ragged last split included): bit-identical run to run, and both
+    the split and the unsplit op (no scratch) within the fp32 tolerance."""
+    M, N, K = mnk
+    rng = np.random.default_rng(M + N + K + kind)
+    x = rng.standard_normal((M, K)).astype(np.float32)
+    w = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
+    resid = rng.standard_normal((M, N)).astype(np.float32)
+    xd, wd, rd = (torch.from_numpy(a).cuda() for a in (x, w, resid))
+    scratch = torch.empty(S.sarathi_linear_scratch_bytes(M, N), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    outs = []
+    for use_scratch in (True, True, False):
+        out = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+        S.sarathi_linear(S.F32, kind, M, N, K, xd.data_ptr(), wd.data_ptr(), rd.data_ptr(), out.data_ptr(),
+                         scratch.data_ptr() if use_scratch else 0, scratch.numel() if use_scratch else 0, stream)
+        outs.append(out)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits_of(outs[0]), bits_of(outs[1])), "split-K result differs between runs"
+    ref = resid.astype(np.float64) + oracle.linear(x, w)
+    for o in outs[0], outs[2]:
+        err = rel_err(from_dev(o), ref)
+        log(f"fp32 split-K kind {kind} {mnk}: err {err:.3e}")
+        assert err <= TOL["f32"]
+
+
 # ============================================================================ whole layer
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
