@@ -124,6 +124,39 @@ def per_call_ms(make_call, stream, steps):
     return [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
 
 
+def oracle_cpu_baseline(oracle, shp, w, kv_layer, ob, x, T, budget_s=25.0, one_core_max_s=45.0):
+    """The oracle on the host cores: one full layer call of the workload,
+    one untimed warm-up, then the median of up to 3 calls within budget_s
+    with every BLAS thread, and one call limited to a single thread (skipped
+    when it would take longer than one_core_max_s)."""
+    import numpy as np
+    from threadpoolctl import threadpool_info, threadpool_limits
+    kv = kv_layer.copy()          # the oracle writes the new K/V rows in place (same values every call)
+    run = lambda: oracle.layer_forward(shp, w, kv, ob, x)
+    run()
+    times = []
+    t0 = time.perf_counter()
+    while len(times) < 3 and time.perf_counter() - t0 < budget_s:
+        t1 = time.perf_counter()
+        run()
+        times.append(time.perf_counter() - t1)
+    blas = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+    threads = int(max([i.get("num_threads", 1) for i in blas], default=1))
+    lib = ", ".join(f"{i.get('internal_api')} {i.get('version')}" for i in blas) or "none"
+    t_cpu = float(np.median(times))
+    one = None
+    if t_cpu * threads <= one_core_max_s:
+        with threadpool_limits(limits=1, user_api="blas"):
+            t1 = time.perf_counter()
+            run()
+            one = time.perf_counter() - t1
+    return {"value": round(T / t_cpu, 2), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"one full layer call of the same workload ({T} rows), float64 NumPy, median of "
+                      f"{len(times)} runs of {t_cpu:.2f}s after one warm-up; host affinity "
+                      f"{len(os.sched_getaffinity(0))} cpus",
+            "blas": lib, "one_core_value": round(T / one, 2) if one else None}
+
+
 def chunk_key_ranges(offset, C, nh, qblock=128, tau_min=4):
     """Key ranges per 128-row query block of a chunk, as the runtime plans
     them: tiles of 64 keys cut into ranges of at most tau tiles, tau chosen
@@ -344,21 +377,8 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
-        from threadpoolctl import threadpool_info
         ob = oracle.OracleBatch(b.prefill_slot, b.chunk_offset, C, list(b.decode_slots), list(b.decode_ctx))
-        times = []
-        t_start = time.perf_counter()
-        while len(times) < 3 and (time.perf_counter() - t_start) < 25.0:
-            kvc = inst.kv[0]
-            t1 = time.perf_counter()
-            oracle.layer_forward(shp, inst.weights[0], kvc.copy() if not times else kvc, ob, inst.x)
-            times.append(time.perf_counter() - t1)
-        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"],
-                           default=1)
-        t_cpu = float(np.median(times))
-        cpu = {"value": round(T / t_cpu, 2), "unit": "tokens/s", "cores": int(blas_threads), "kind": "oracle",
-               "sample": f"one full layer call of the same workload ({T} rows), float64 NumPy, median of "
-                         f"{len(times)} runs of {t_cpu:.2f}s; host affinity {len(os.sched_getaffinity(0))} cpus"}
+        cpu = oracle_cpu_baseline(oracle, shp, inst.weights[0], inst.kv[0], ob, inst.x, T)
 
     stack = None
     if not args.no_stack:
