@@ -1,0 +1,66 @@
+"""Host-side checks of the benchmark's bookkeeping (no GPU): the algorithmic
+work per stage against closed forms, the mirror of the chunk key-range plan,
+the one-GPU guard and the oracle timing helper."""
+import os
+import subprocess
+import sys
+
+import numpy as np
+
+import bench
+import oracle
+import workloads as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_stage_work_matches_closed_forms_for_the_llama13b_layer():
+    w = wl.WORKLOADS["llama13b-layer-bf16-c256-b64"]
+    b, s = wl.draw_batch(np.random.Generator(np.random.PCG64(w.seed)), w.batch), w.shape   # generate()'s first draw
+    T, H, F, QD = b.n_tokens, s.hidden, s.ffn, s.n_heads * s.head_dim
+    work = bench.stage_work(s, b)
+    lin = ("preproj", "postproj", "ffn_ln1", "ffn_ln2")
+    flops = sum(work[k][0] for k in lin)
+    assert flops == 2 * T * H * (3 * QD + QD + 2 * F) + 2 * T * F * H
+    assert abs(flops / 1e9 - 203.0) < 0.05                      # 320 rows of the LLaMA-13B layer
+    weight_bytes = 2 * (3 * QD * H + H * QD + 2 * F * H + H * F)
+    assert abs(weight_bytes / 1e6 - 634.4) < 0.05
+    act = sum(work[k][1] for k in lin) - weight_bytes
+    assert 0 < act < 0.1 * weight_bytes                          # activations are a small share at 320 rows
+    keys = int(np.sum(b.decode_ctx.astype(np.int64) + 1))
+    dec_flops, dec_bytes = work["decode_attention"]
+    assert dec_flops == 4.0 * keys * QD
+    assert dec_bytes >= keys * 2 * QD * 2                         # every cached K and V byte once
+    pairs = b.chunk_len * b.chunk_offset + b.chunk_len * (b.chunk_len + 1) // 2
+    assert work["chunk_attention"][0] == 4.0 * pairs * QD         # masked pairs not counted
+
+
+def test_chunk_key_ranges_cover_every_tile():
+    for off, C, nh in [(512, 256, 40), (2048, 512, 52), (1792, 256, 96), (0, 1, 4), (100, 37, 4), (60000, 100, 2)]:
+        ranges = bench.chunk_key_ranges(off, C, nh)
+        nq = -(-C // 128)
+        assert len(ranges) == nq
+        for qb, n in enumerate(ranges):
+            tiles = -(-(off + min((qb + 1) * 128, C)) // 64)      # key tiles the block's last row needs
+            assert 1 <= n <= tiles
+            assert -(-tiles // n) >= 4 or n == 1                    # ranges of at least 4 tiles unless unsplit
+    assert bench.chunk_key_ranges(0, 0, 4) == []
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_oracle_cpu_baseline_fields():
+    w = wl.TINY
+    inst = wl.generate(w)
+    b = inst.batch
+    ob = oracle.OracleBatch(b.prefill_slot, b.chunk_offset, b.chunk_len, list(b.decode_slots), list(b.decode_ctx))
+    cpu = bench.oracle_cpu_baseline(oracle, w.shape, inst.weights[0], inst.kv[0], ob, inst.x, b.n_tokens)
+    assert cpu["kind"] == "oracle" and cpu["unit"] == "tokens/s"
+    assert cpu["value"] > 0 and cpu["cores"] >= 1
+    assert cpu["one_core_value"] is not None and cpu["one_core_value"] > 0
+    assert "median of" in cpu["sample"]
