@@ -453,6 +453,45 @@ def test_model_step_consecutive_steps(dtype):
         assert err_y <= TOL[dtype] and err_kv <= TOL[dtype]
 
 
+def test_model_step_forty_layers_f32_chained():
+    """A 40-layer fp32 stack (tiny layer shapes) over two consecutive steps
+    through sarathi_model_step: every layer's output, run layer by layer on
+    the same batch, against the oracle chained through all 40 layers on its
+    own outputs (one iteration of the model, Sec. 4.5), at the fp32
+    tolerance; the model step equals the layer-by-layer run bit for bit; the
+    K/V written at every layer matches the oracle's."""
+    L, Sx, n_slots = 40, 256, 6
+    shape = dataclasses.replace(_tiny_shape("f32"), n_layers=L)
+    b0 = wl.Batch(prefill_slot=3, chunk_offset=0, chunk_len=48, decode_slots=np.array([0, 5, 1], np.int32),
+                  decode_ctx=np.array([7, 130, 64], np.int32))
+    inst = wl.make_instance(shape, b0, max_seq_len=Sx, n_slots=n_slots, seed=41, n_layers=L)
+    dm = DeviceModel(inst)
+    okv = inst.kv.astype(np.float64)
+    rng = np.random.default_rng(9)
+    for step in range(2):
+        b = wl.Batch(prefill_slot=3, chunk_offset=48 * step, chunk_len=48, decode_slots=b0.decode_slots,
+                     decode_ctx=b0.decode_ctx + step)
+        xs = inst.x if step == 0 else rng.standard_normal(inst.x.shape).astype(np.float32)
+        x_dev = to_dev(xs, "f32")
+        y_ms = dm.step(b, x_dev)
+        hs = [x_dev]
+        for layer in range(L):
+            hs.append(dm.layer(layer, b, hs[-1]))
+        torch.cuda.synchronize()
+        assert torch.equal(y_ms, hs[-1]), "model step differs from the layer-by-layer run"
+        outs = oracle.model_step(shape, inst.weights, okv, oracle_batch(b), xs)
+        errs = [rel_err(from_dev(hs[layer + 1]), outs[layer].y) for layer in range(L)]
+        kvf = from_dev(dm.kv_dev)
+        kv_errs = []
+        for layer in range(L):
+            got = np.stack([kvf[layer, s, :, :, p, :] for s, p in zip(outs[layer].slots, outs[layer].positions)])
+            kv_errs.append(rel_err(got[:, 0], outs[layer].k_new))
+            kv_errs.append(rel_err(got[:, 1], outs[layer].v_new))
+        log(f"40-layer f32 step {step}: y error by layer (first, 20th, last) {errs[0]:.2e} {errs[19]:.2e} "
+            f"{errs[-1]:.2e}; max over layers {max(errs):.2e}; K/V max {max(kv_errs):.2e}")
+        assert max(errs) <= TOL["f32"] and max(kv_errs) <= TOL["f32"]
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_piggybacked_decode_equals_decode_alone(dtype):
     """Sec. 4.3: a decode piggybacked on a chunk gives the same row as the same
