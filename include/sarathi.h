@@ -245,6 +245,27 @@ int sarathi_model_step(const sarathi_model_cfg* cfg, const sarathi_layer_weights
                        void* hip_stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * sarathi_hybrid_layer_forward with its workspace in a static device array
+ * of SARATHI_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it
+ * runs on until the process ends (looked up on the first call on a device).
+ * The call allocates nothing; the caller still passes x_in, x_out, the
+ * weights and the KV cache, with the same meaning, layout and KV contract
+ * as sarathi_hybrid_layer_forward, and gets the same results.
+ * Every call on one GPU shares that GPU's array: calls that overlap on one
+ * GPU (different streams, or different host threads without ordering) race.
+ * Errors: as sarathi_hybrid_layer_forward; ENOSPC when the batch needs more
+ * workspace than the array holds (sarathi_workspace_bytes(cfg, T, B,
+ * max_seq_len) > SARATHI_NOALLOC_SCRATCH_BYTES); EHIP if the array's device
+ * address cannot be looked up.
+ */
+#define SARATHI_NOALLOC_SCRATCH_BYTES (160ull << 20)
+int sarathi_hybrid_layer_forward_noalloc(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w,
+                                         sarathi_kv* kv, int layer, const sarathi_hybrid_batch* batch,
+                                         const void* x_in, void* x_out, void* hip_stream);
+
+/*
  * sarathi_hybrid_layer_forward / sarathi_model_step over a mixed batch (any
  * number of prompt chunks, Sec. 5.2's mixed batching): the linear ops run
  * over all rows, each chunk's attention over its own slot, each decode over

@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libsarathi.so")
 SOURCES = ["runtime.cpp", "scheduler.cpp", "elementwise.hip", "gemm.hip", "chunk_attention.hip", "decode_attention.hip",
-           "attention_combine.hip"]
+           "attention_combine.hip", "noalloc.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

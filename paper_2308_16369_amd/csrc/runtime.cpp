@@ -15,6 +15,7 @@
 
 #include "host_error.h"
 #include "kernels.h"
+#include "runtime_internal.h"
 #include "sarathi.h"
 
 using namespace sarathi;
@@ -501,9 +502,9 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
   return SARATHI_OK;
 }
 
-int prepare(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, int n_w, sarathi_kv* kv,
-            const BatchDesc& batch, const void* x_in, void* x_out, void* ws, size_t ws_bytes,
-            Plan* plan, Layout* L) {
+// Every check of a call that does not involve the workspace.
+int check_call(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, int n_w, const sarathi_kv* kv,
+               const BatchDesc& batch, const void* x_in, const void* x_out) {
   int rc = check_cfg(cfg);
   if (rc) return rc;
   if (!kv) return fail(SARATHI_EINVAL, "kv is NULL");
@@ -515,10 +516,18 @@ int prepare(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, int n_
     if (rc) return rc;
   }
   if (!x_in || !x_out) return fail(SARATHI_EINVAL, "x_in / x_out is NULL");
-  if (!ws) return fail(SARATHI_EINVAL, "workspace is NULL");
   if (x_in == x_out) return fail(SARATHI_EINVAL, "x_in and x_out alias");
-  if (!aligned16(x_in) || !aligned16(x_out) || !aligned16(ws))
-    return fail(SARATHI_EINVAL, "x_in, x_out and ws must be 16-byte aligned");
+  if (!aligned16(x_in) || !aligned16(x_out)) return fail(SARATHI_EINVAL, "x_in, x_out and ws must be 16-byte aligned");
+  return SARATHI_OK;
+}
+
+int prepare(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, int n_w, sarathi_kv* kv,
+            const BatchDesc& batch, const void* x_in, void* x_out, void* ws, size_t ws_bytes,
+            Plan* plan, Layout* L) {
+  int rc = check_call(cfg, w, n_w, kv, batch, x_in, x_out);
+  if (rc) return rc;
+  if (!ws) return fail(SARATHI_EINVAL, "workspace is NULL");
+  if (!aligned16(ws)) return fail(SARATHI_EINVAL, "x_in, x_out and ws must be 16-byte aligned");
   const int T = batch.rows();
   *L = make_layout(cfg, T, (int)batch.chunks.size(), kv->max_seq_len);
   if (ws_bytes < L->total)
@@ -540,6 +549,19 @@ int prepare(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, int n_
 }
 
 }  // namespace
+
+int sarathi::hybrid_check_noalloc(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, const sarathi_kv* kv,
+                                  int layer, const sarathi_hybrid_batch* batch, const void* x_in, const void* x_out,
+                                  size_t* need) {
+  BatchDesc b;
+  int rc = from_hybrid(batch, &b);
+  if (rc) return rc;
+  rc = check_call(cfg, w, 1, kv, b, x_in, x_out);
+  if (rc) return rc;
+  if (layer < 0 || layer >= cfg->n_layers) return fail(SARATHI_EINVAL, "layer %d outside [0, %d)", layer, cfg->n_layers);
+  *need = make_layout(cfg, b.rows(), (int)b.chunks.size(), kv->max_seq_len).total;
+  return SARATHI_OK;
+}
 
 // ============================================================================ C-ABI
 

@@ -19,6 +19,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libsarathi.so")
 
 OK, EINVAL, ERANGE, ENOSPC, EUNSUPPORTED, EHIP = 0, -1, -2, -3, -4, -5
+NOALLOC_SCRATCH_BYTES = 160 << 20   # SARATHI_NOALLOC_SCRATCH_BYTES
 F32, BF16 = 0, 1
 NORM_RMS, NORM_LAYER = 0, 1
 ACT_SWIGLU, ACT_GELU = 0, 1
@@ -102,6 +103,10 @@ EXPORTS = {
     "sarathi_hybrid_layer_forward": (ct.c_int, [ct.POINTER(sarathi_model_cfg), ct.POINTER(sarathi_layer_weights),
                                                 ct.c_void_p, ct.c_int, ct.POINTER(sarathi_hybrid_batch),
                                                 ct.c_void_p, ct.c_void_p, ct.c_void_p, ct.c_size_t, ct.c_void_p]),
+    "sarathi_hybrid_layer_forward_noalloc": (ct.c_int, [ct.POINTER(sarathi_model_cfg),
+                                                        ct.POINTER(sarathi_layer_weights), ct.c_void_p, ct.c_int,
+                                                        ct.POINTER(sarathi_hybrid_batch), ct.c_void_p, ct.c_void_p,
+                                                        ct.c_void_p]),
     "sarathi_model_step": (ct.c_int, [ct.POINTER(sarathi_model_cfg), ct.POINTER(sarathi_layer_weights),
                                       ct.c_void_p, ct.POINTER(sarathi_hybrid_batch), ct.c_void_p, ct.c_void_p,
                                       ct.c_void_p, ct.c_size_t, ct.c_void_p]),
@@ -239,6 +244,14 @@ def sarathi_hybrid_layer_forward(cfg, weights: sarathi_layer_weights, kv: KV, la
     rc = lib().sarathi_hybrid_layer_forward(ct.byref(cfg), ct.byref(weights), kv.handle, layer, ct.byref(batch),
                                             ct.c_void_p(x_in), ct.c_void_p(x_out), ct.c_void_p(ws), ws_bytes,
                                             ct.c_void_p(stream))
+    return _check(rc) if check else rc
+
+
+def sarathi_hybrid_layer_forward_noalloc(cfg, weights: sarathi_layer_weights, kv: KV, layer: int, batch, x_in: int,
+                                         x_out: int, stream: int = 0, check: bool = True) -> int:
+    rc = lib().sarathi_hybrid_layer_forward_noalloc(ct.byref(cfg), ct.byref(weights), kv.handle, layer,
+                                                    ct.byref(batch), ct.c_void_p(x_in), ct.c_void_p(x_out),
+                                                    ct.c_void_p(stream))
     return _check(rc) if check else rc
 
 

@@ -261,3 +261,24 @@ def test_linear_tile_queries_and_validation(lib):
     assert call(K=96) == S.EUNSUPPORTED                  # not a multiple of 64
     assert call(kind=9) == S.EINVAL
     assert call(kind=S.LINEAR_RESID) == S.EINVAL         # resid is NULL
+
+
+def test_noalloc_validates_and_rejects_batches_beyond_its_scratch(lib):
+    s = Setup(lib)
+    b, keep = S.make_batch(1, 0, 4, [2, 2], [3, 4])                # duplicate decode slot
+    assert S.sarathi_hybrid_layer_forward_noalloc(s.cfg, s.w, s.kv, 0, b, 0x200000, 0x300000,
+                                                  check=False) == S.EINVAL
+    b, keep = S.make_batch(1, 0, 4, [3], [10])
+    assert S.sarathi_hybrid_layer_forward_noalloc(s.cfg, s.w, s.kv, 5, b, 0x200000, 0x300000,
+                                                  check=False) == S.EINVAL      # layer out of range
+    assert S.sarathi_hybrid_layer_forward_noalloc(s.cfg, s.w, s.kv, 0, b, 0x200000, 0x200000,
+                                                  check=False) == S.EINVAL      # x_in == x_out
+    # a batch whose workspace exceeds the static scratch
+    n_slots, S_ = 2, 1 << 20
+    cfg = tiny_cfg(dtype=S.BF16)
+    kv = S.sarathi_kv_alloc(cfg, n_slots, S_, FAKE_DEV, S.sarathi_kv_bytes(cfg, n_slots, S_))
+    w = S.make_weights({k: FAKE_DEV for k in ("norm1_g", "w_qkv", "w_o", "norm2_g", "w_up", "w_down")})
+    big = S.make_batch(0, 0, 100000, [1], [5])
+    assert S.sarathi_workspace_bytes(cfg, 100001, 1, S_) > S.NOALLOC_SCRATCH_BYTES
+    rc = S.sarathi_hybrid_layer_forward_noalloc(cfg, w, kv, 0, big[0], 0x200000, 0x40000000, check=False)
+    assert rc == S.ENOSPC and "static scratch" in S.sarathi_last_error()
