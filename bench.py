@@ -22,6 +22,8 @@ import os
 import sys
 import time
 
+import numpy as np
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
@@ -46,7 +48,7 @@ def parse():
     return ap.parse_args()
 
 
-def bench_stack(steps: int, warmup: int):
+def bench_stack(steps: int, warmup: int, cpu_baseline: bool = True):
     """Model step of the 40-layer LLaMA-13B-shaped stack (chunk 256 + 48
     decodes of context U[512, 2048], KV for 49 slots x 2112 positions):
     time per step, per layer, and the decode accounting of Sec. 5.1.1 against
@@ -101,10 +103,15 @@ def bench_stack(steps: int, warmup: int):
            "tokens_per_s": round(T / (ms * 1e-3), 1), "ms_per_layer": round(ms / L, 5),
            "prefill_only_ms_per_step": round(ms_p, 4), "decode_only_ms_per_step": round(ms_d, 4),
            "decode_tokens_per_s_hybrid": round(1e3 / t_h, 1) if t_h > 0 else None,
+           "decode_tokens_per_s_hybrid_accounting": "Sec. 5.1.1: B / (t_hybrid - t_prefill_only)",
            "decode_tokens_per_s_decode_only": round(1e3 / t_b, 1),
            "decode_speedup": round(t_b / t_h, 3) if t_h > 0 else None}
+    out["decode_tokens_per_s_plain"] = round(B / (ms * 1e-3), 1)
     del st, ws
     torch.cuda.empty_cache()
+    if cpu_baseline:
+        import oracle
+        out["cpu_baseline"] = oracle_stack_baseline(oracle, shp, b, L)
     return out
 
 
@@ -157,6 +164,61 @@ def oracle_cpu_baseline(oracle, shp, w, kv_layer, ob, x, T, budget_s=25.0, one_c
             "blas": lib, "one_core_value": round(T / one, 2) if one else None}
 
 
+class _SlotKV:
+    """One layer's KV cache as the oracle indexes it ([slot, kv, head, pos,
+    d]), holding only positions [0, n) of the slots a batch touches."""
+
+    def __init__(self, need: dict, nh: int, d: int):
+        self.blk = {s: np.full((2, nh, n, d), 0.5, np.float32) for s, n in need.items()}
+
+    def __getitem__(self, idx):
+        return self.blk[int(idx[0])][tuple(idx[1:])]
+
+    def __setitem__(self, idx, val):
+        self.blk[int(idx[0])][tuple(idx[1:])] = val
+
+
+def oracle_stack_baseline(oracle, shp, b, n_layers: int, budget_s: float = 8.0):
+    """The oracle on the host cores for the 40-layer stack: one layer of the
+    stack's step-0 batch (same rows, chunk and decode contexts; constant
+    weights and cache values of the same shapes -- the time of the plain
+    NumPy arithmetic does not depend on the values), timed after one
+    warm-up call (median of the calls that fit budget_s, at least one), then
+    multiplied by the layer count and labelled as extrapolated."""
+    from threadpoolctl import threadpool_info
+    rng = np.random.default_rng(0)
+    H, nh, d, F = shp.hidden, shp.n_heads, shp.head_dim, shp.ffn
+    f32 = lambda *sh: np.full(sh, 0.01, np.float32)
+    w = {"w_qkv": f32(3 * nh * d, H), "w_o": f32(H, nh * d), "w_up": f32(shp.up_rows, H), "w_down": f32(H, F),
+         "norm1_g": np.ones(H, np.float32), "norm2_g": np.ones(H, np.float32)}
+    need = {}
+    if b.chunk_len:
+        need[int(b.prefill_slot)] = int(b.chunk_offset) + int(b.chunk_len)
+    for s_, c in zip(b.decode_slots, b.decode_ctx):
+        need[int(s_)] = int(c) + 1
+    ob = oracle.OracleBatch(b.prefill_slot, b.chunk_offset, b.chunk_len, list(b.decode_slots), list(b.decode_ctx))
+    x = rng.random((b.n_tokens, H), dtype=np.float32) - 0.5
+    kv = _SlotKV(need, nh, d)
+    run = lambda: oracle.layer_forward(shp, w, kv, ob, x)
+    run()
+    times = []
+    t0 = time.perf_counter()
+    while len(times) < 3 and time.perf_counter() - t0 < budget_s:
+        t1 = time.perf_counter()
+        run()
+        times.append(time.perf_counter() - t1)
+    blas = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+    threads = int(max([i.get("num_threads", 1) for i in blas], default=1))
+    t_layer = float(np.median(times))
+    t_step = t_layer * n_layers
+    return {"value": round(b.n_tokens / t_step, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "extrapolated": True,
+            "sample": f"one layer of the stack's step-0 batch ({b.n_tokens} rows), float64 NumPy, median of "
+                      f"{len(times)} runs of {t_layer:.2f}s after one warm-up, times {n_layers} layers "
+                      f"(extrapolated, not run); host affinity {len(os.sched_getaffinity(0))} cpus",
+            "ms_per_step": round(t_step * 1e3, 1)}
+
+
 def chunk_key_ranges(offset, C, nh, qblock=128, tau_min=4):
     """Key ranges per 128-row query block of a chunk, as the runtime plans
     them: tiles of 64 keys cut into ranges of at most tau tiles, tau chosen
@@ -175,12 +237,14 @@ def chunk_key_ranges(offset, C, nh, qblock=128, tau_min=4):
     return [-(-t // tau) for t in qt]
 
 
-def stage_work(shp, b, S_stats=None):
-    """Algorithmic FLOPs and HBM bytes of each stage of one layer call.
-
-    Bytes count what the method must move once: weights once, KV read once
-    per query set, activations once in and once out; FLOPs count 2 per
-    multiply-add, attention pairs only where the mask allows them."""
+def stage_work(shp, b):
+    """Algorithmic FLOPs and HBM bytes of each stage of one layer call --
+    only what the method itself must compute and move (Sec. 4.3's fused
+    linear ops and separate attention): weights once, KV read once per query
+    set, activations once in and once out, attention output rows counted
+    with the attention that produces them; FLOPs count 2 per multiply-add,
+    attention pairs only where the mask allows them.  The combine of
+    attention key-splits is implementation overhead (no method bytes)."""
     T, C, B = b.n_tokens, b.chunk_len, b.n_decodes
     H, nh, hd, F = shp.hidden, shp.n_heads, shp.head_dim, shp.ffn
     QD = nh * hd
@@ -194,20 +258,41 @@ def stage_work(shp, b, S_stats=None):
     w["norm_1"] = (0.0, 2 * T * H * es + T * H * 4)
     w["preproj"] = (2.0 * T * H * 3 * QD, 3 * QD * H * es + T * H * es + T * 3 * QD * es)
     w["rope_kv_append"] = (0.0, 2 * T * 3 * QD * es + T * QD * es)
-    # key-split partials (hd + 2 fp32 per head): decode rows split every 512
-    # keys; chunk rows in 128-row query blocks, each block's 64-key tiles cut
-    # into near-equal ranges (the runtime's work decomposition)
-    dec_parts = sum(-(-(c + 1) // 512) for c in ctx)
-    pre_parts = sum(128 * n for n in chunk_key_ranges(b.chunk_offset, C, nh))
-    part_bytes = nh * (hd + 2) * 4
-    w["chunk_attention"] = (4.0 * pre_pairs * hd * nh, pre_keys * 2 * QD * es + C * QD * es + pre_parts * part_bytes)
-    w["decode_attention"] = (4.0 * dec_keys * hd * nh, dec_keys * 2 * QD * es + B * QD * es + dec_parts * part_bytes)
-    w["attention_combine"] = (0.0, (dec_parts + pre_parts) * part_bytes + T * QD * es)
+    w["chunk_attention"] = (4.0 * pre_pairs * hd * nh, pre_keys * 2 * QD * es + 2 * C * QD * es)
+    w["decode_attention"] = (4.0 * dec_keys * hd * nh, dec_keys * 2 * QD * es + 2 * B * QD * es)
+    w["attention_combine"] = (0.0, 0.0)
     w["postproj"] = (2.0 * T * QD * H, H * QD * es + T * QD * es + T * H * es + T * H * 4)
     w["norm_2"] = (0.0, T * H * 4 + T * H * es + T * H * 4)
     w["ffn_ln1"] = (2.0 * T * H * up_rows, up_rows * H * es + T * H * es + T * F * es)
     w["ffn_ln2"] = (2.0 * T * F * H, H * F * es + T * F * es + T * H * 4 + T * H * es)
     return w
+
+
+def stage_overhead(shp, b, split_counts=None):
+    """HBM bytes each stage moves beyond the method's own (stage_work):
+    fp32 key-split partials of the attention (hd + 2 floats per row and head:
+    decode rows split every 512 keys; chunk rows in 128-row query blocks, each
+    block's 64-key tiles cut into near-equal ranges -- the runtime's work
+    decomposition), written by the attention kernels and read by the
+    combine; and the fp32 split-K partials of postproj and ffn_ln2
+    (split_counts: stage -> K-splits of its matmul), written by the matmul
+    and read back by its reduction pass."""
+    T, C, B = b.n_tokens, b.chunk_len, b.n_decodes
+    H, nh, hd = shp.hidden, shp.n_heads, shp.head_dim
+    QD = nh * hd
+    es = 2 if shp.dtype == "bf16" else 4
+    ctx = [int(c) for c in b.decode_ctx]
+    dec_parts = sum(-(-(c + 1) // 512) for c in ctx)
+    pre_parts = sum(128 * n for n in chunk_key_ranges(b.chunk_offset, C, nh))
+    part_bytes = nh * (hd + 2) * 4
+    o = {k: 0.0 for k in BOUND}
+    o["chunk_attention"] = pre_parts * part_bytes
+    o["decode_attention"] = dec_parts * part_bytes
+    o["attention_combine"] = (dec_parts + pre_parts) * part_bytes + T * QD * es
+    for st, ns in (split_counts or {}).items():
+        if ns > 1:
+            o[st] += 2.0 * ns * T * H * 4
+    return o
 
 
 def counter_traffic(stage: str, workload: str):
@@ -228,7 +313,7 @@ def counter_traffic(stage: str, workload: str):
 
 
 BOUND = {"norm_1": "hbm", "preproj": "mfma", "rope_kv_append": "hbm", "chunk_attention": "mfma",
-         "decode_attention": "hbm", "attention_combine": "hbm", "postproj": "mfma", "norm_2": "hbm",
+         "decode_attention": "hbm", "attention_combine": "overhead", "postproj": "mfma", "norm_2": "hbm",
          "ffn_ln1": "mfma", "ffn_ln2": "mfma"}
 
 
@@ -330,6 +415,8 @@ def main():
         extra = {
             "prefill_only_ms": round(ms_p, 5), "decode_only_ms": round(ms_d, 5),
             "decode_tokens_per_s_hybrid": round(1e3 / t_dec_h, 1) if t_dec_h > 0 else None,
+            "decode_tokens_per_s_hybrid_accounting": "Sec. 5.1.1: B / (t_hybrid - t_prefill_only)",
+            "decode_tokens_per_s_plain": round(B / (ms_plain * 1e-3), 1),
             "decode_tokens_per_s_decode_only": round(1e3 / t_dec_b, 1),
             "decode_speedup": round(t_dec_b / t_dec_h, 3) if t_dec_h > 0 else None,
         }
@@ -342,8 +429,16 @@ def main():
         torch.cuda.synchronize()
         del a, c
 
-    # ---- rooflines per stage
+    # ---- rooflines per stage (method FLOPs and bytes), with each stage's
+    # implementation overhead traffic reported beside them
     work = stage_work(shp, b)
+    dt_abi = S.BF16 if shp.dtype == "bf16" else S.F32
+    split_scratch = S.sarathi_layer_split_scratch_bytes(cfg, T)
+    QD = shp.n_heads * shp.head_dim
+    splits = {"postproj": S.sarathi_linear_plan(dt_abi, S.LINEAR_RESID, T, shp.hidden, QD, split_scratch)[2],
+              "ffn_ln2": S.sarathi_linear_plan(dt_abi, S.LINEAR_RESID_F32IN, T, shp.hidden, shp.ffn,
+                                               split_scratch)[2]}
+    over = stage_overhead(shp, b, splits)
     peak_flops = PEAK_BF16_TFLOPS if shp.dtype == "bf16" else PEAK_F32_TFLOPS
     kernels = {}
     for name, t in stages.items():
@@ -355,8 +450,11 @@ def main():
         gb = by / sec / 1e9
         kernels[name] = {"ms": round(t, 5), "tflops": round(tf, 2), "gbps": round(gb, 1),
                          "mfma_frac": round(tf / peak_flops, 4), "hbm_frac": round(gb / PEAK_HBM_GBPS, 4),
-                         "bound": BOUND[name]}
-    dom = max(kernels, key=lambda k: kernels[k]["ms"])
+                         "bound": BOUND[name], "overhead_bytes": round(over[name]),
+                         "gbps_with_overhead": round((by + over[name]) / sec / 1e9, 1)}
+        if name in splits:
+            kernels[name]["k_splits"] = splits[name]
+    dom = max((k for k in kernels if kernels[k]["bound"] != "overhead"), key=lambda k: kernels[k]["ms"])
     dk = kernels[dom]
     if dk["bound"] == "mfma":
         roof = {"bound": "mfma", "achieved": dk["tflops"], "peak": peak_flops, "unit": "TFLOP/s",
@@ -368,6 +466,7 @@ def main():
     roof["traffic"] = counter_traffic(dom, w.name)
     # layer roofline: every stage at the larger of its MFMA and HBM times
     roof_ms = sum(max(fl / (peak_flops * 1e12), by / (PEAK_HBM_GBPS * 1e9)) for fl, by in work.values()) * 1e3
+    over_total = sum(over.values())
     lin = ["preproj", "postproj", "ffn_ln1", "ffn_ln2"]
     lin_ms = sum(kernels[k]["ms"] for k in lin if k in kernels)
     lin_flops = sum(work[k][0] for k in lin)
@@ -385,7 +484,7 @@ def main():
         del kv_t, wdev, ws
         torch.cuda.empty_cache()
         t_s = time.time()
-        stack = bench_stack(args.stack_steps, 2)
+        stack = bench_stack(args.stack_steps, 2, cpu_baseline=not args.no_cpu_baseline)
         print(f"# stack measured in {time.time() - t_s:.1f}s: {stack['ms_per_step']} ms per step",
               file=sys.stderr, flush=True)
 
@@ -408,7 +507,8 @@ def main():
                    "ctx_range": [w.batch.ctx_lo, w.batch.ctx_hi], "rows": T, "parallelism": "none (1 GPU)"},
         "roofline": roof,
         "cpu_baseline": cpu,
-        "layer_roofline": {"ms": round(roof_ms, 5), "frac": round(roof_ms / ms_plain, 4)},
+        "layer_roofline": {"ms": round(roof_ms, 5), "frac": round(roof_ms / ms_plain, 4),
+                           "overhead_bytes": round(over_total)},
         "ms_per_call_p10_p50_p90": [round(float(np.percentile(per_call, q)), 5) for q in (10, 50, 90)],
         "ms_per_step_with_stage_events": round(ms, 5),
         "wall_ms_per_step": round(wall_ms, 5),

@@ -311,6 +311,22 @@ int sarathi_linear(int dtype, int kind, int M, int N, int K, const void* x, cons
                    void* hip_stream);
 
 /*
+ * The block shape (*bm rows of x by *bn rows of W) and K-split count that
+ * sarathi_linear would run the op with, given scratch_bytes of split-K
+ * scratch; nothing is launched.  sarathi_layer_split_scratch_bytes(cfg, T)
+ * is the split-K scratch a layer call of T rows gives its two residual ops
+ * (postproj, ffn_ln2), so the plan of a layer's op is
+ * sarathi_linear_plan(..., sarathi_layer_split_scratch_bytes(cfg, T), ...).
+ * For measurement: the fp32 partials of a split op (n_split x M x N x 4
+ * bytes written, then read back) are traffic beyond the method's own.
+ * Errors: EINVAL (NULL outputs, bad kind or sizes), EUNSUPPORTED (dtype,
+ * K not a multiple of 8).
+ */
+int sarathi_linear_plan(int dtype, int kind, int M, int N, int K, size_t scratch_bytes, int* bm, int* bn,
+                        int* n_split);
+size_t sarathi_layer_split_scratch_bytes(const sarathi_model_cfg* cfg, int n_tokens);
+
+/*
  * Tile shapes of the bf16 matmul kernel, for tests and tuning:
  * sarathi_linear_tile_count() shapes, shape t = *bm rows of x by *bn rows of
  * W per block (sarathi_linear_tile_shape returns EINVAL for t out of range).

@@ -14,7 +14,12 @@ through the C-ABI:
   the attention alone and for the whole layer, c from 64 to 512;
 * decode piggybacking: for a chunk of c tokens and B decodes, the decode time
   per token of the hybrid batch (hybrid minus prefill-only time, over B)
-  against a decode-only batch (the accounting of Sec. 5.1.1).
+  against a decode-only batch (the accounting of Sec. 5.1.1);
+* the per-token prefill and decode times of Sec. 4.3's table, re-run on the
+  whole 40-layer LLaMA-13B model: a prefill-only iteration of 1024 tokens, a
+  decode-only iteration of 4 decodes at sequence length 1024, and a
+  decode-maximal iteration of one 1021-token chunk plus 3 decodes, each split
+  into linear-op, attention and other time.
 
 Inputs are seeded synthetic tensors drawn on the device (weights
 0.02 * N(0,1), activations and cached K/V N(0,1)); only timing is measured
@@ -34,6 +39,12 @@ from dataclasses import dataclass
 from typing import Callable, Dict, List, Optional, Sequence, Tuple
 
 LINEAR_STAGES = ("preproj", "postproj", "ffn_ln1", "ffn_ln2")
+ATTENTION_STAGES = ("chunk_attention", "decode_attention", "attention_combine")
+
+# Sec. 4.3's table (LLaMA-13B, A6000): total ms of one iteration of the whole
+# model, linear / attention / total, for the three batch kinds (context only).
+PAPER_TABLE2_A6000 = {"prefill_only": (224.8, 10.0, 234.8), "decode_only": (44.28, 5.68, 49.96),
+                      "decode_maximal": (223.2, 15.2, 238.4)}
 
 
 def chunk_plan(prompt_len: int, chunk: int) -> List[Tuple[int, int]]:
@@ -210,6 +221,119 @@ def piggyback(r: LayerRunner, chunks: Sequence[int], decodes: Sequence[int], ctx
     return out
 
 
+def table2_batches(seq_len: int = 1024, decodes: int = 4):
+    """The three iterations of Sec. 4.3's table at sequence length
+    ``seq_len``: prefill-only (one prompt of seq_len tokens, slot 0),
+    decode-only (``decodes`` decodes whose new token sits at position
+    seq_len - 1, slots 1..decodes) and decode-maximal (a chunk of
+    seq_len - (decodes - 1) tokens plus decodes - 1 of those decodes, seq_len
+    rows in all)."""
+    dec = decodes - 1
+    return {"prefill_only": Batch(0, 0, seq_len, [], []),
+            "decode_only": Batch(-1, 0, 0, list(range(1, decodes + 1)), [seq_len - 1] * decodes),
+            "decode_maximal": Batch(0, 0, seq_len - dec, list(range(1, dec + 1)), [seq_len - 1] * dec),
+            "prefill_only_chunk": Batch(0, 0, seq_len - dec, [], [])}
+
+
+def table2(shape, n_layers: int = 40, seq_len: int = 1024, decodes: int = 4, iters: int = 10) -> dict:
+    """Per-token prefill and decode time of the whole model (Sec. 4.3's
+    table), with each iteration split into linear ops, attention and the rest
+    from per-stage HIP events (summed over layers; the events add a few
+    microseconds per stage, so the split is of the profiled run and the
+    total of an unprofiled one).  Decode time per token follows Sec. 5.1.1:
+    decode-only time / batch, and (decode-maximal - prefill-only) / decodes."""
+    import torch
+
+    from workloads.stack import generate_model_on_device
+    from . import sarathi as S
+
+    dm = generate_model_on_device(shape, n_layers, decodes + 1, seq_len)
+    cfg = S.make_cfg(hidden=shape.hidden, n_heads=shape.n_heads, head_dim=shape.head_dim, ffn=shape.ffn,
+                     n_layers=n_layers, norm=S.NORM_RMS if shape.norm == "rms" else S.NORM_LAYER,
+                     act=S.ACT_SWIGLU if shape.act == "swiglu" else S.ACT_GELU, rope=int(shape.rope),
+                     rope_base=shape.rope_base, eps=shape.eps, dtype=S.BF16 if shape.dtype == "bf16" else S.F32)
+    kv = S.sarathi_kv_alloc(cfg, decodes + 1, seq_len, dm.kv.data_ptr(), dm.kv.numel() * dm.kv.element_size())
+    wabi = [S.make_weights({k: t.data_ptr() for k, t in lw.items()}) for lw in dm.weights]
+    ws_bytes = S.sarathi_workspace_bytes(cfg, seq_len, decodes, seq_len)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    x = torch.empty((seq_len, shape.hidden), dtype=dm.kv.dtype, device="cuda").normal_(0.0, 1.0)
+    y = torch.empty_like(x)
+    stream = torch.cuda.current_stream()
+    out = {}
+    for name, b in table2_batches(seq_len, decodes).items():
+        bb, keep = S.make_batch(b.prefill_slot, b.chunk_offset, b.chunk_len, b.decode_slots, b.decode_ctx)
+        call = lambda: S.sarathi_model_step(cfg, wabi, kv, bb, x.data_ptr(), y.data_ptr(), ws.data_ptr(), ws_bytes,
+                                            stream.cuda_stream)
+        for _ in range(2):
+            call()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(iters):
+            call()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        total = e0.elapsed_time(e1) / iters
+        S.sarathi_profile_begin(3 * n_layers)
+        for _ in range(3):
+            call()
+        torch.cuda.synchronize()
+        st, n = S.sarathi_profile_end()
+        st = {k: v / 3 for k, v in st.items()}
+        lin = sum(st[k] for k in LINEAR_STAGES)
+        att = sum(st[k] for k in ATTENTION_STAGES)
+        out[name] = {"rows": b.n_tokens, "prefill_tokens": b.chunk_len, "decode_tokens": len(b.decode_slots),
+                     "total_ms": round(total, 4), "linear_ms": round(lin, 4), "attention_ms": round(att, 4),
+                     "other_ms": round(sum(st.values()) - lin - att, 4),
+                     "profiled_total_ms": round(sum(st.values()), 4)}
+    p, d, h, pc = (out[k]["total_ms"] for k in ("prefill_only", "decode_only", "decode_maximal",
+                                                 "prefill_only_chunk"))
+    dec = decodes - 1
+    out["per_token_ms"] = {
+        "prefill": round(p / seq_len, 5),
+        "decode_baseline": round(d / decodes, 5),
+        "decode_hybrid": round((h - p) / dec, 5),
+        "decode_hybrid_same_chunk": round((h - pc) / dec, 5),
+    }
+    out["decode_speedup"] = round((d / decodes) / ((h - p) / dec), 3) if h > p else None
+    out["decode_speedup_same_chunk"] = round((d / decodes) / ((h - pc) / dec), 3) if h > pc else None
+    out["layers"], out["seq_len"], out["decodes"] = n_layers, seq_len, decodes
+    del ws, dm
+    torch.cuda.empty_cache()
+    return out
+
+
+def table2_markdown(t: dict) -> str:
+    rows = [("prefill_only", f"prefill-only ({t['seq_len']} tokens)"),
+            ("decode_only", f"decode-only ({t['decodes']} decodes at {t['seq_len']})"),
+            ("decode_maximal", f"decode-maximal ({t['seq_len'] - t['decodes'] + 1} + {t['decodes'] - 1})"),
+            ("prefill_only_chunk", f"prefill-only ({t['seq_len'] - t['decodes'] + 1} tokens)")]
+    L = [f"## Per-token prefill and decode time, whole {t['layers']}-layer model (Sec. 4.3's table)", "",
+         "Linear = preproj + postproj + ffn_ln1 + ffn_ln2 (split-K reductions included), attention = chunk + "
+         "decode attention + combine, other = norms and the rotary/KV append when it runs alone; the split is "
+         "from a run with per-stage events (a few us each), the total from one without.  The paper's A6000 "
+         "values are context, not a target.", "",
+         "| iteration | rows | linear ms | attention ms | other ms | total ms | paper A6000 linear / attn / total ms |",
+         "|---|---|---|---|---|---|---|"]
+    for k, label in rows:
+        e = t[k]
+        pap = PAPER_TABLE2_A6000.get(k)
+        ps = " / ".join(f"{v:g}" for v in pap) if pap else "—"
+        L.append(f"| {label} | {e['rows']} | {e['linear_ms']:.3f} | {e['attention_ms']:.3f} | {e['other_ms']:.3f} | "
+                 f"{e['total_ms']:.3f} | {ps} |")
+    pt = t["per_token_ms"]
+    L += ["", "| per-token time | this GPU (ms) | paper A6000 (ms) |", "|---|---|---|",
+          f"| prefill (prefill-only time / {t['seq_len']}) | {pt['prefill']:.5f} | 0.229 |",
+          f"| decode, decode-only batch (time / {t['decodes']}) | {pt['decode_baseline']:.4f} | 12.49 |",
+          f"| decode, decode-maximal batch ((decode-maximal - prefill-only {t['seq_len']}) / "
+          f"{t['decodes'] - 1}) | {pt['decode_hybrid']:.4f} | 1.2 |",
+          f"| decode, decode-maximal batch ((decode-maximal - prefill-only {t['seq_len'] - t['decodes'] + 1}) / "
+          f"{t['decodes'] - 1}) | {pt['decode_hybrid_same_chunk']:.4f} | — |",
+          "", f"Decode speedup: {t['decode_speedup']} (paper: 12.49 / 1.2 = 10.4); against the prefill-only time of "
+              f"the same {t['seq_len'] - t['decodes'] + 1}-token chunk: {t['decode_speedup_same_chunk']}.", ""]
+    return "\n".join(L) + "\n"
+
+
 def to_markdown(res: dict) -> str:
     L = [f"# Chunk-size ablation and tile quantization: {res['workload']}", "",
          f"Command: `{res['command']}`", "", "## Tile quantization (prefill-only layer call of T rows)", "",
@@ -232,7 +356,10 @@ def to_markdown(res: dict) -> str:
         L.append(f"| {e['chunk']} | {e['decodes']} | {e['rows']} | {e['hybrid_ms']:.4f} | {e['prefill_only_ms']:.4f} | "
                  f"{e['decode_only_ms']:.4f} | {e['decode_us_per_token_hybrid']:.2f} | "
                  f"{e['decode_us_per_token_decode_only']:.2f} | {e['decode_speedup']} |")
-    return "\n".join(L) + "\n"
+    out = "\n".join(L) + "\n"
+    if res.get("table2"):
+        out += "\n" + table2_markdown(res["table2"])
+    return out
 
 
 def main(argv: Optional[Sequence[str]] = None) -> int:
@@ -241,6 +368,8 @@ def main(argv: Optional[Sequence[str]] = None) -> int:
     ap.add_argument("--json", default=None)
     ap.add_argument("--md", default=None)
     ap.add_argument("--quick", action="store_true", help="a few points of each sweep")
+    ap.add_argument("--table2-only", action="store_true", help="only the whole-model per-token table")
+    ap.add_argument("--no-table2", action="store_true", help="skip the whole-model per-token table")
     args = ap.parse_args(argv)
 
     import torch
@@ -271,6 +400,20 @@ def main(argv: Optional[Sequence[str]] = None) -> int:
     log("inputs on the device")
     res = {"workload": f"{args.workload}-layer-{shape.dtype}", "command":
            "python -m paper_2308_16369_amd.ablation " + " ".join(argv if argv is not None else sys.argv[1:])}
+    if args.table2_only:
+        del r
+        torch.cuda.empty_cache()
+        res["table2"] = table2(shape, n_layers=40 if args.workload == "llama13b" else 2)
+        log("table 2 done")
+        if args.json:
+            with open(args.json, "w") as f:
+                json.dump(res, f, indent=1)
+        if args.md:
+            with open(args.md, "w") as f:
+                f.write(f"# Per-token prefill and decode time: {res['workload']}\n\nCommand: `{res['command']}`\n\n"
+                        + table2_markdown(res["table2"]))
+        print(json.dumps(res["table2"]["per_token_ms"]))
+        return 0
     res["tile_quantization"] = tile_quantization(r, lengths)
     log("tile quantization done")
     res["chunking_overhead"] = chunking_overhead(r, prompts, chunks)
@@ -278,6 +421,11 @@ def main(argv: Optional[Sequence[str]] = None) -> int:
     res["piggyback_ctx"], res["piggyback_offset"] = ctx, offset
     res["piggyback"] = piggyback(r, pig_chunks, pig_dec, ctx, offset)
     log("piggyback done")
+    if not args.no_table2:
+        del r
+        torch.cuda.empty_cache()
+        res["table2"] = table2(shape, n_layers=40 if args.workload == "llama13b" else 2)
+        log("table 2 done")
     if args.json:
         with open(args.json, "w") as f:
             json.dump(res, f, indent=1)

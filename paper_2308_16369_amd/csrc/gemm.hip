@@ -720,7 +720,9 @@ bool linear_tile_shape(int tile, int* bm, int* bn) {
   return true;
 }
 
-hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s, int force_tile, int force_split) {
+hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s, int force_tile, int force_split,
+                         LinearPlan* plan) {
+  if (plan) *plan = LinearPlan{0, 0, 0};
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
   GemmP p{};
   p.A = a.x; p.W = a.w; p.M = a.M; p.N = a.N; p.K = a.K;
@@ -741,11 +743,19 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s, int forc
         p.k_split = (steps + ns - 1) / ns * 64;
         p.n_split = (a.K + p.k_split - 1) / p.k_split;
         p.out = a.parts;
+        if (plan) {
+          *plan = LinearPlan{64, 64, p.n_split};
+          return hipSuccess;
+        }
         hipError_t e = run_f32<EPI_PARTIAL>(p, s);
         if (e != hipSuccess) return e;
         return launch_split_reduce(0, a.kind == LIN_RESID_F32IN, a.kind == LIN_RESID, a.resid, a.parts, p.n_split,
                                    (size_t)a.M * a.N, a.out, s);
       }
+    }
+    if (plan) {
+      *plan = LinearPlan{64, 64, 1};
+      return hipSuccess;
     }
     switch (a.kind) {
       case LIN_PLAIN: return run_f32<EPI_STORE>(p, s);
@@ -831,6 +841,10 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s, int forc
     }
   }
   p.n_tiles = p.tiles_m * p.tiles_n * p.n_split;
+  if (plan) {
+    *plan = LinearPlan{BM, BN, p.n_split};
+    return hipSuccess;
+  }
   hipError_t e;
   if (ws) {
     e = run_ws_epi(epi, cfg, p, s);

@@ -79,7 +79,14 @@ constexpr int MAX_SPLIT = 6;   // split-K partials: at most MAX_SPLIT x [M, N] f
 // force_tile >= 0 (bf16, K a multiple of 64): run that producer/consumer tile
 // shape with force_split K-splits (residual kinds with scratch) instead of the
 // cost model's choice.
-hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s, int force_tile = -1, int force_split = 0);
+// With plan non-null nothing is launched: *plan receives the block shape and
+// K-split count the op would run with (bm = bn = 0 for the fp32 kernel's
+// 64 x 64 tiles is reported as 64, 64).
+struct LinearPlan {
+  int bm, bn, n_split;
+};
+hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s, int force_tile = -1, int force_split = 0,
+                         LinearPlan* plan = nullptr);
 int linear_tile_count();
 bool linear_tile_shape(int tile, int* bm, int* bn);
 

@@ -788,6 +788,31 @@ int sarathi_linear(int dtype, int kind, int M, int N, int K, const void* x, cons
   return linear_common(dtype, kind, M, N, K, x, w, resid, out, scratch, scratch_bytes, hip_stream, -1, 0);
 }
 
+int sarathi_linear_plan(int dtype, int kind, int M, int N, int K, size_t scratch_bytes, int* bm, int* bn,
+                        int* n_split) {
+  if (!bm || !bn || !n_split) return fail(SARATHI_EINVAL, "NULL pointer");
+  if (dtype != SARATHI_F32 && dtype != SARATHI_BF16) return fail(SARATHI_EUNSUPPORTED, "dtype %d", dtype);
+  if (kind < SARATHI_LINEAR_PLAIN || kind > SARATHI_LINEAR_GELU) return fail(SARATHI_EINVAL, "kind %d", kind);
+  if (M < 1 || N < 1 || K < 1) return fail(SARATHI_EINVAL, "M, N, K must be positive");
+  if (K % 8) return fail(SARATHI_EUNSUPPORTED, "K %d must be a multiple of 8", K);
+  LinearArgs a{};
+  a.kind = kind; a.M = M; a.N = N; a.K = K;
+  static float dummy;   // plan only: the scratch is never touched
+  if ((kind == SARATHI_LINEAR_RESID || kind == SARATHI_LINEAR_RESID_F32IN) && scratch_bytes >= 4) {
+    a.parts = &dummy;
+    a.parts_cap = scratch_bytes / 4;
+  }
+  LinearPlan pl{};
+  if (launch_linear(dtype, a, nullptr, -1, 0, &pl) != hipSuccess) return fail(SARATHI_EINVAL, "no plan for this op");
+  *bm = pl.bm; *bn = pl.bn; *n_split = pl.n_split;
+  return SARATHI_OK;
+}
+
+size_t sarathi_layer_split_scratch_bytes(const sarathi_model_cfg* cfg, int n_tokens) {
+  if (!cfg || n_tokens < 1) return 0;
+  return (size_t)MAX_SPLIT * std::min(n_tokens, PARTS_ROWS) * cfg->hidden * 4;
+}
+
 int sarathi_linear_tile_count(void) { return linear_tile_count(); }
 
 int sarathi_linear_tile_shape(int tile, int* bm, int* bn) {

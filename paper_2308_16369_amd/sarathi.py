@@ -124,6 +124,9 @@ EXPORTS = {
     "sarathi_linear_scratch_bytes": (ct.c_size_t, [ct.c_int, ct.c_int]),
     "sarathi_linear": (ct.c_int, [ct.c_int, ct.c_int, ct.c_int, ct.c_int, ct.c_int, ct.c_void_p, ct.c_void_p,
                                   ct.c_void_p, ct.c_void_p, ct.c_void_p, ct.c_size_t, ct.c_void_p]),
+    "sarathi_linear_plan": (ct.c_int, [ct.c_int, ct.c_int, ct.c_int, ct.c_int, ct.c_int, ct.c_size_t,
+                                       ct.POINTER(ct.c_int), ct.POINTER(ct.c_int), ct.POINTER(ct.c_int)]),
+    "sarathi_layer_split_scratch_bytes": (ct.c_size_t, [ct.POINTER(sarathi_model_cfg), ct.c_int]),
     "sarathi_linear_tile_count": (ct.c_int, []),
     "sarathi_linear_tile_shape": (ct.c_int, [ct.c_int, ct.POINTER(ct.c_int), ct.POINTER(ct.c_int)]),
     "sarathi_linear_tiled": (ct.c_int, [ct.c_int, ct.c_int, ct.c_int, ct.c_int, ct.c_void_p, ct.c_void_p,
@@ -328,6 +331,17 @@ def sarathi_linear(dtype, kind, M, N, K, x: int, w: int, resid: int, out: int, s
     rc = lib().sarathi_linear(dtype, kind, M, N, K, ct.c_void_p(x), ct.c_void_p(w), ct.c_void_p(resid or None),
                               ct.c_void_p(out), ct.c_void_p(scratch or None), scratch_bytes, ct.c_void_p(stream))
     return _check(rc) if check else rc
+
+
+def sarathi_linear_plan(dtype, kind, M, N, K, scratch_bytes: int = 0):
+    """(bm, bn, n_split) that sarathi_linear would run the op with."""
+    bm, bn, ns = ct.c_int(), ct.c_int(), ct.c_int()
+    _check(lib().sarathi_linear_plan(dtype, kind, M, N, K, scratch_bytes, ct.byref(bm), ct.byref(bn), ct.byref(ns)))
+    return bm.value, bn.value, ns.value
+
+
+def sarathi_layer_split_scratch_bytes(cfg: sarathi_model_cfg, n_tokens: int) -> int:
+    return int(lib().sarathi_layer_split_scratch_bytes(ct.byref(cfg), n_tokens))
 
 
 def sarathi_linear_tile_count() -> int:

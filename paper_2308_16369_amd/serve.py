@@ -27,6 +27,7 @@ import sys
 import time
 from typing import List, Optional, Sequence, Tuple
 
+from . import accounting
 from . import sarathi as S
 
 POLICY_NAMES = {S.POLICY_DECODE_MAXIMAL: "decode-maximal", S.POLICY_PREFILL_DECODE: "prefill/decode",
@@ -188,7 +189,13 @@ def sweep(m: ServeModel, seq_len: int, ratios: Sequence[float], chunks: Sequence
 
 def to_markdown(res: dict) -> str:
     L = [f"# End-to-end throughput vs P:D: {res['workload']}", "", f"Command: `{res['command']}`", "",
-         res["note"], "",
+         res["note"], ""]
+    eq = res.get("batch_equation")
+    if eq:
+        L += [f"B from Sec. 4.3.1: floor((M_G - headroom - M_S) / (L m_kv)) = floor(({eq['mem_gpu'] / 1e9:.1f} - "
+              f"{eq['headroom'] / 1e9:.1f} - {eq['mem_params'] / 1e9:.2f} GB) / ({eq['seq_len']} x "
+              f"{eq['kv_bytes_per_token'] / 1e3:.1f} KB)) = {eq['B']}.", ""]
+    L += [
          "| seq | P | D | P:D | B | C | C/(B-1) | decode-maximal tok/s | baseline tok/s | speedup | "
          "mixed tok/s (speedup) | hybrid / prefill-only / decode-only iterations |",
          "|---|---|---|---|---|---|---|---|---|---|---|---|"]
@@ -201,10 +208,29 @@ def to_markdown(res: dict) -> str:
     return "\n".join(L) + "\n"
 
 
+def equation_batch(shape, n_layers: int, seq_len: int, mem_gpu: int, headroom: int = 0) -> dict:
+    """The decode batch of Sec. 4.3.1, B = floor((M_G - M_S) / (L * m_kv)):
+    M_G the device memory (less ``headroom`` for activations and the
+    workspace), M_S the bytes of the model's weights, L the sequence length
+    and m_kv the K and V bytes of one token over all layers."""
+    es = 2 if shape.dtype == "bf16" else 4
+    H, nh, d, F = shape.hidden, shape.n_heads, shape.head_dim, shape.ffn
+    per_layer = (3 * nh * d * H + H * nh * d + shape.up_rows * H + H * F + 2 * H) * es
+    m_s = n_layers * per_layer
+    m_kv = n_layers * 2 * nh * d * es
+    b = accounting.max_decode_batch(mem_gpu - headroom, m_s, seq_len, m_kv)
+    return {"B": b, "mem_gpu": mem_gpu, "headroom": headroom, "mem_params": m_s, "kv_bytes_per_token": m_kv,
+            "seq_len": seq_len}
+
+
 def main(argv: Optional[Sequence[str]] = None) -> int:
     ap = argparse.ArgumentParser(description="decode-maximal batching vs prefill/decode batches, end to end")
     ap.add_argument("--layers", type=int, default=40)
-    ap.add_argument("--batch", type=int, default=18)
+    ap.add_argument("--batch", type=int, default=0,
+                    help="decode batch B (default: the Sec. 4.3.1 equation over the device memory)")
+    ap.add_argument("--mem-gb", type=float, default=0.0,
+                    help="device memory M_G for the B equation, GB (default: the device's total)")
+    ap.add_argument("--max-batch", type=int, default=0, help="cap on the equation's B (0: none)")
     ap.add_argument("--seq", type=int, nargs="+", default=[1024])
     ap.add_argument("--chunks", type=int, nargs="+", default=[128, 256, 512])
     ap.add_argument("--ratios", type=float, nargs="+", default=[1, 2, 4, 8, 14, 28, 50, 100])
@@ -221,6 +247,16 @@ def main(argv: Optional[Sequence[str]] = None) -> int:
 
     assert torch.cuda.is_available(), "the serving study runs on a GPU"
     shape = wl.LLAMA13B_LAYER.shape
+    eq = None
+    if args.batch <= 0:
+        mem = int(args.mem_gb * 1e9) if args.mem_gb > 0 else torch.cuda.get_device_properties(0).total_memory
+        eq = equation_batch(shape, args.layers, max(args.seq), mem, headroom=8 << 30)
+        args.batch = eq["B"] if args.max_batch <= 0 else min(eq["B"], args.max_batch)
+        print(f"# B = {args.batch} from Sec. 4.3.1: floor(({eq['mem_gpu'] / 1e9:.1f} GB - {eq['headroom'] / 1e9:.1f} GB "
+              f"headroom - {eq['mem_params'] / 1e9:.2f} GB weights) / ({eq['seq_len']} x "
+              f"{eq['kv_bytes_per_token'] / 1e3:.1f} KB)) = {eq['B']}"
+              + (f", capped at {args.max_batch}" if args.max_batch > 0 and args.max_batch < eq["B"] else ""),
+              file=sys.stderr, flush=True)
     n_req = args.requests or 2 * args.batch
     max_seq = max(args.seq)
     max_tokens = max(max(args.seq), max(args.chunks) + args.batch)
@@ -238,7 +274,7 @@ def main(argv: Optional[Sequence[str]] = None) -> int:
            "note": f"{n_req} requests of equal P and D per run, B = {args.batch} resident at once; baseline = "
                    f"whole-prompt prefill-only iterations then decode-only iterations (Sec. 5.1); synthetic "
                    f"hidden states stand in for tokens.",
-           "sweep": []}
+           "batch_equation": eq, "sweep": []}
     for seq in args.seq:
         res["sweep"] += sweep(m, seq, args.ratios, args.chunks, args.batch, n_req, log, mixed=args.mixed)
     if args.json:

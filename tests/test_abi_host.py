@@ -282,3 +282,17 @@ def test_noalloc_validates_and_rejects_batches_beyond_its_scratch(lib):
     assert S.sarathi_workspace_bytes(cfg, 100001, 1, S_) > S.NOALLOC_SCRATCH_BYTES
     rc = S.sarathi_hybrid_layer_forward_noalloc(cfg, w, kv, 0, big[0], 0x200000, 0x40000000, check=False)
     assert rc == S.ENOSPC and "static scratch" in S.sarathi_last_error()
+
+
+def test_linear_plan_reports_split_choice():
+    from paper_2308_16369_amd import sarathi as S
+    # residual op of the LLaMA-13B layer at 320 rows: split over K when the scratch allows it
+    cfg = S.make_cfg(hidden=5120, n_heads=40, head_dim=128, ffn=13824, n_layers=1, dtype=S.BF16)
+    scratch = S.sarathi_layer_split_scratch_bytes(cfg, 320)
+    assert scratch == 6 * 320 * 5120 * 4
+    bm, bn, ns = S.sarathi_linear_plan(S.BF16, S.LINEAR_RESID, 320, 5120, 5120, scratch)
+    assert bm > 0 and bn > 0 and 1 <= ns <= 6
+    assert S.sarathi_linear_plan(S.BF16, S.LINEAR_RESID, 320, 5120, 5120, 0)[2] == 1     # no scratch: no split
+    assert S.sarathi_linear_plan(S.BF16, S.LINEAR_PLAIN, 320, 15360, 5120, scratch)[2] == 1
+    with pytest.raises(S.SarathiError):
+        S.sarathi_linear_plan(S.BF16, 9, 320, 5120, 5120, 0)

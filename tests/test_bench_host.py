@@ -64,3 +64,29 @@ def test_oracle_cpu_baseline_fields():
     assert cpu["value"] > 0 and cpu["cores"] >= 1
     assert cpu["one_core_value"] is not None and cpu["one_core_value"] > 0
     assert "median of" in cpu["sample"]
+
+
+def test_stage_overhead_is_separate_from_method_bytes():
+    w = wl.WORKLOADS["llama13b-layer-bf16-c256-b64"]
+    b, s = wl.draw_batch(np.random.Generator(np.random.PCG64(w.seed)), w.batch), w.shape
+    T, H, QD = b.n_tokens, s.hidden, s.n_heads * s.head_dim
+    work = bench.stage_work(s, b)
+    assert work["attention_combine"] == (0.0, 0.0)             # the combine is not the method's work
+    over = bench.stage_overhead(s, b, {"postproj": 3, "ffn_ln2": 1})
+    assert over["postproj"] == 2.0 * 3 * T * H * 4               # fp32 partials written and read back
+    assert over["ffn_ln2"] == 0.0                                 # no split, no partials
+    part_row = s.n_heads * (s.head_dim + 2) * 4
+    dec_parts = sum(-(-(int(c) + 1) // 512) for c in b.decode_ctx)
+    assert over["decode_attention"] == dec_parts * part_row
+    assert over["attention_combine"] == over["decode_attention"] + over["chunk_attention"] + T * QD * 2
+    for k in ("preproj", "ffn_ln1", "norm_1", "norm_2"):
+        assert over[k] == 0.0
+
+
+def test_stack_oracle_baseline_is_labelled_extrapolated():
+    w = wl.TINY
+    b = wl.draw_batch(np.random.Generator(np.random.PCG64(w.seed)), w.batch)
+    r = bench.oracle_stack_baseline(oracle, w.shape, b, 40, budget_s=0.5)
+    assert r["extrapolated"] is True and r["kind"] == "oracle"
+    assert r["value"] > 0 and "times 40 layers" in r["sample"]
+    assert abs(r["ms_per_step"] - b.n_tokens / r["value"] * 1e3) < 0.01 * r["ms_per_step"] + 1

@@ -188,3 +188,18 @@ def test_argument_errors():
         s.commit()
     assert ei.value.code == S.ENOSPC
     s.submit(10, 6)                                   # P + D == max_seq_len is allowed
+
+
+def test_serving_batch_from_the_memory_equation():
+    """Sec. 4.3.1: B = floor((M_G - M_S) / (L m_kv)) for the LLaMA-13B shape
+    (40 layers, 634 MB of weights per layer, 0.8 MB of K/V per token)."""
+    import workloads as wl
+    from paper_2308_16369_amd.serve import equation_batch
+    shape = wl.LLAMA13B_LAYER.shape
+    eq = equation_batch(shape, 40, 1024, 288 * 10**9, headroom=8 << 30)
+    m_s = 40 * 2 * (3 * 5120 * 5120 + 5120 * 5120 + 2 * 13824 * 5120 + 5120 * 13824 + 2 * 5120)
+    m_kv = 40 * 2 * 5120 * 2
+    assert eq["mem_params"] == m_s and eq["kv_bytes_per_token"] == m_kv
+    assert eq["B"] == (288 * 10**9 - (8 << 30) - m_s) // (1024 * m_kv)
+    # an A6000-sized device (48 GB, no headroom) gives the paper's order of magnitude
+    assert 20 <= equation_batch(shape, 40, 1024, 48 * 10**9)["B"] <= 30

@@ -101,3 +101,27 @@ def generate_layer_on_device(shp, n_slots: int, max_seq_len: int, seed: int = 0)
         lw["norm1_b"] = torch.empty(H, dtype=dt, device="cuda").normal_(0.0, 0.02, generator=g)
         lw["norm2_b"] = torch.empty(H, dtype=dt, device="cuda").normal_(0.0, 0.02, generator=g)
     return DeviceLayer(shape=shp, kv=kv, weights=lw)
+
+
+@dataclass
+class DeviceModel:
+    """Weights of ``n_layers`` layers and a KV cache on the device (timing)."""
+    shape: "object"
+    kv: "object"                 # torch [L, n_slots, 2, nh, S, d]
+    weights: List[dict]
+
+
+def generate_model_on_device(shp, n_layers: int, n_slots: int, max_seq_len: int, seed: int = 0) -> DeviceModel:
+    """``n_layers`` layers of weights plus a KV cache whose every position
+    holds a finite N(0,1) value, drawn with torch's seeded generator (the
+    same distributions as :func:`generate_layer_on_device`)."""
+    import torch
+
+    layers = [generate_layer_on_device(shp, 1, 1, seed + 1000 * i).weights for i in range(n_layers)]
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    dt = torch.bfloat16 if shp.dtype == "bf16" else torch.float32
+    kv = torch.empty((n_layers, n_slots, 2, shp.n_heads, max_seq_len, shp.head_dim), dtype=dt, device="cuda")
+    for layer in range(n_layers):
+        kv[layer].normal_(0.0, 1.0, generator=g)
+    return DeviceModel(shape=shp, kv=kv, weights=layers)
