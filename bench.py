@@ -219,24 +219,6 @@ def oracle_stack_baseline(oracle, shp, b, n_layers: int, budget_s: float = 8.0):
             "ms_per_step": round(t_step * 1e3, 1)}
 
 
-def chunk_key_ranges(offset, C, nh, qblock=128, tau_min=4):
-    """Key ranges per 128-row query block of a chunk, as the runtime plans
-    them: tiles of 64 keys cut into ranges of at most tau tiles, tau chosen
-    to minimise rounds of 512 blocks x (longest range + 4)."""
-    if C <= 0:
-        return []
-    qt = [-(-(offset + min((qb + 1) * qblock, C)) // 64) for qb in range(-(-C // qblock))]
-    best, tau, cand = float("inf"), tau_min, tau_min
-    while cand <= max(max(qt), tau_min):
-        ns = [-(-t // cand) for t in qt]
-        longest = max(-(-t // n) for t, n in zip(qt, ns))
-        cost = -(-(sum(ns) * nh) // 512) * (longest + 4)
-        if cost <= best:
-            best, tau = cost, cand
-        cand += max(1, cand // 4)
-    return [-(-t // tau) for t in qt]
-
-
 def stage_work(shp, b):
     """Algorithmic FLOPs and HBM bytes of each stage of one layer call --
     only what the method itself must compute and move (Sec. 4.3's fused
@@ -268,27 +250,24 @@ def stage_work(shp, b):
     return w
 
 
-def stage_overhead(shp, b, split_counts=None):
-    """HBM bytes each stage moves beyond the method's own (stage_work):
-    fp32 key-split partials of the attention (hd + 2 floats per row and head:
-    decode rows split every 512 keys; chunk rows in 128-row query blocks, each
-    block's 64-key tiles cut into near-equal ranges -- the runtime's work
-    decomposition), written by the attention kernels and read by the
-    combine; and the fp32 split-K partials of postproj and ffn_ln2
-    (split_counts: stage -> K-splits of its matmul), written by the matmul
-    and read back by its reduction pass."""
-    T, C, B = b.n_tokens, b.chunk_len, b.n_decodes
+def stage_overhead(shp, b, attn_plan, split_counts=None):
+    """HBM bytes each stage moves beyond the method's own (stage_work): the
+    fp32 key-split partials of the attention (hd + 4 floats per row and head;
+    attn_plan: the library's sarathi_attention_plan of the batch -- the rows
+    each attention kernel writes and the combine pass reads back, plus the
+    output rows the combine writes), and the fp32 split-K partials of
+    postproj and ffn_ln2 (split_counts: stage -> K-splits of its matmul),
+    written by the matmul and read back by its reduction pass."""
+    T = b.n_tokens
     H, nh, hd = shp.hidden, shp.n_heads, shp.head_dim
-    QD = nh * hd
     es = 2 if shp.dtype == "bf16" else 4
-    ctx = [int(c) for c in b.decode_ctx]
-    dec_parts = sum(-(-(c + 1) // 512) for c in ctx)
-    pre_parts = sum(128 * n for n in chunk_key_ranges(b.chunk_offset, C, nh))
-    part_bytes = nh * (hd + 2) * 4
+    part_bytes = nh * (hd + 4) * 4
+    dec_rows = attn_plan["decode_items"]
     o = {k: 0.0 for k in BOUND}
-    o["chunk_attention"] = pre_parts * part_bytes
-    o["decode_attention"] = dec_parts * part_bytes
-    o["attention_combine"] = (dec_parts + pre_parts) * part_bytes + T * QD * es
+    o["chunk_attention"] = (attn_plan["partial_rows_written"] - dec_rows) * part_bytes
+    o["decode_attention"] = dec_rows * part_bytes
+    o["attention_combine"] = (attn_plan["partial_rows_read"] * part_bytes
+                              + attn_plan["combine_rows"] * nh * hd * es)
     for st, ns in (split_counts or {}).items():
         if ns > 1:
             o[st] += 2.0 * ns * T * H * 4
@@ -438,7 +417,8 @@ def main():
     splits = {"postproj": S.sarathi_linear_plan(dt_abi, S.LINEAR_RESID, T, shp.hidden, QD, split_scratch)[2],
               "ffn_ln2": S.sarathi_linear_plan(dt_abi, S.LINEAR_RESID_F32IN, T, shp.hidden, shp.ffn,
                                                split_scratch)[2]}
-    over = stage_overhead(shp, b, splits)
+    bb_plan, keep_plan = S.make_batch(b.prefill_slot, b.chunk_offset, C, list(b.decode_slots), list(b.decode_ctx))
+    over = stage_overhead(shp, b, S.sarathi_attention_plan(cfg, bb_plan), splits)
     peak_flops = PEAK_BF16_TFLOPS if shp.dtype == "bf16" else PEAK_F32_TFLOPS
     kernels = {}
     for name, t in stages.items():

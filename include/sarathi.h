@@ -205,6 +205,25 @@ size_t sarathi_mixed_workspace_bytes(const sarathi_model_cfg* cfg, int max_token
 int sarathi_mixed_workspace_layout(const sarathi_model_cfg* cfg, int n_tokens, int n_chunks,
                                    int max_seq_len, sarathi_ws_layout* out);
 
+/*
+ * How a layer call splits a hybrid batch's attention into work items (for
+ * measurement; nothing is launched, the batch is checked against cfg only):
+ * the chunk-attention and decode-attention work items per head, the rows of
+ * fp32 key-split partials they write (hd + 4 floats per row and head; a
+ * chunk item that covers every key of its rows writes the attention output
+ * directly), and the partial rows the combine pass reads back.  Errors:
+ * EINVAL (NULL arguments, malformed batch).
+ */
+typedef struct {
+  int chunk_items;
+  int decode_items;
+  long partial_rows_written;
+  long partial_rows_read;
+  int combine_rows;
+} sarathi_attn_plan;
+int sarathi_attention_plan(const sarathi_model_cfg* cfg, const sarathi_hybrid_batch* batch,
+                           sarathi_attn_plan* out);
+
 /* ------------------------------------------------------------------ forward */
 /*
  * One decoder layer over a hybrid batch (Sec. 4.3; layer `layer` of the KV

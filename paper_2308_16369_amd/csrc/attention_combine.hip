@@ -15,17 +15,18 @@ namespace sarathi {
 template <typename T, int D>
 __global__ __launch_bounds__(256) void attn_combine_kernel(CombineArgs a) {
   constexpr int E = D / 64, U = 8;
-  const int r = blockIdx.x, lane = threadIdx.x & 63;
+  const int r = a.row0 + blockIdx.x, lane = threadIdx.x & 63;
   const int h = blockIdx.y * 4 + (threadIdx.x >> 6);
   if (h >= a.nh) return;
   const int start = a.comb[3 * r], cnt = a.comb[3 * r + 1], stride = a.comb[3 * r + 2];
-  auto src_of = [&](int j) { return a.part + ((size_t)(start + j * stride) * a.nh + h) * (D + 2); };
+  if (cnt == 0) return;   // written directly by its attention kernel
+  auto src_of = [&](int j) { return a.part + ((size_t)(start + j * stride) * a.nh + h) * (D + PART_O); };
   float v[U][E];
   auto load_group = [&](int j0) {
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int e = 0; e < E; ++e) v[u][e] = (j0 + u < cnt) ? src_of(j0 + u)[2 + lane + 64 * e] : 0.f;
+      for (int e = 0; e < E; ++e) v[u][e] = (j0 + u < cnt) ? src_of(j0 + u)[PART_O + lane + 64 * e] : 0.f;
   };
   // first chunk of up to 64 splits: (m, l) per lane, o of the first U splits
   const int n0 = min(64, cnt);
@@ -70,8 +71,8 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(CombineArgs a) {
 }
 
 hipError_t launch_attn_combine(int dtype, const CombineArgs& a, hipStream_t s) {
-  if (a.n_rows <= 0) return hipSuccess;
-  dim3 grid(a.n_rows, (a.nh + 3) / 4);
+  if (a.n_rows <= a.row0) return hipSuccess;
+  dim3 grid(a.n_rows - a.row0, (a.nh + 3) / 4);
   if (dtype == 0) {
     if (a.hd == 128) hipLaunchKernelGGL((attn_combine_kernel<float, 128>), grid, dim3(256), 0, s, a);
     else hipLaunchKernelGGL((attn_combine_kernel<float, 64>), grid, dim3(256), 0, s, a);

@@ -1,15 +1,17 @@
 // Attention of the prompt chunk(s) of the hybrid batch, run separately from the
-// decodes (Sec. 4.3).  It writes per-split partial results (max, sum,
-// unnormalised o) that the combine pass of attention_combine.hip merges per row.
+// decodes (Sec. 4.3).  A work item that sees every key of its rows writes
+// their attention output directly; a key range of a split item is written as
+// a partial result (max, sum, unnormalised o) that the combine pass of
+// attention_combine.hip merges per row.
 //
 // Chunked-prefill attention (bf16, MFMA): the chunk's queries at positions
 // off..off+C-1 attend to the prefill slot's keys 0..position (the earlier
 // chunks' cached keys plus, causally, the chunk's own; Sec. 4.2).  Work item
 // = (block of PREFILL_QBLOCK queries, a range of 64-key tiles), one head per
-// block of PREFILL_QBLOCK / 16 waves x 16 query rows.  K and V tiles of 64
-// keys are staged in a ring of LDS stages by LDS DMA (V read back transposed
-// so P*V takes 16 contiguous bytes per lane); S = Q K^T and O += P V run on
-// v_mfma_f32_16x16x32_bf16 with an fp32 online softmax.
+// block of PREFILL_QBLOCK / 32 waves x 32 query rows.  K and V tiles of 64
+// keys are staged in LDS rings by LDS DMA (V read back transposed so P*V
+// takes 16 contiguous bytes per lane); S = Q K^T and O += P V run on
+// v_mfma_f32_32x32x16_bf16 with an fp32 online softmax.
 #include "kernels.h"
 
 namespace sarathi {
@@ -28,41 +30,102 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
 
 // LDS transpose read (gfx950): within each group of 16 lanes, output lane j
 // element e is element (j % 4) of the 8 bytes addressed by lane 4e + j / 4.
-typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
-__device__ __forceinline__ uint2 lds_read_tr16(const void* p) {
-  const v4i16 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p));
-  return __builtin_bit_cast(uint2, v);
+//
+// The chunk-attention loop issues its LDS reads as inline assembly, with the
+// LDS-counter wait written out (lds_wait): the compiler treats every LDS
+// read as possibly overlapping the tile stages that LDS DMA is still filling
+// and would otherwise wait for all outstanding DMA (vmcnt 0) before the
+// first read of V, which would drain the K/V prefetch every tile.  The
+// stages a tile reads are made complete by the vmcnt wait and barrier at the
+// top of its iteration.  The wait takes the loaded registers as operands so
+// that no use of them can be scheduled before it.
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
+template <int OFF>
+__device__ __forceinline__ u32x2 lds_tr16_asm(uint32_t addr) {
+  u32x2 v;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF));
+  return v;
+}
+template <int OFF>
+__device__ __forceinline__ u32x4 lds_b128_asm(uint32_t addr) {
+  u32x4 v;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF));
+  return v;
+}
+template <int N, typename T>
+__device__ __forceinline__ void lds_wait(T (&r)[N]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < N; ++i) asm volatile("" : "+v"(r[i]));
+}
+// The same, leaving the newest K LDS reads in flight (they complete in issue
+// order): the N registers of the group issued before them have landed.
+template <int K, int N, typename T>
+__device__ __forceinline__ void lds_wait_but(T (&r)[N]) {
+  static_assert(K >= 0 && K < 16, "lgkmcnt range");
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(K) : "memory");
+#pragma unroll
+  for (int i = 0; i < N; ++i) asm volatile("" : "+v"(r[i]));
 }
 
-// One block = one head x (16 * NW queries of the chunk, one split of keys);
-// wave w owns queries w*16..w*16+15.  Per 64-key tile:
-//   S^T = K Q^T  (MFMA: A = K rows from LDS, B = the wave's Q fragments), so
-//     each lane holds 16 scores of ONE query (lane % 16) for keys
-//     nt*16 + 4*(lane/16) + i;
-//   the online softmax runs on that query's own registers (+2 lane shuffles);
-//   O^T += V^T P^T (MFMA: B = the lane's probabilities packed as bf16x8
-//     straight from registers; A = V^T fragments read from the row-major V
-//     tile with LDS transpose reads).  The k order of this product is a
-//     permutation of the 32 keys of a block: lane group g holds keys
-//     4g..4g+3 and 16+4g..16+4g+3, which is what two transpose reads of rows
-//     4g..4g+3 and 16+4g..16+4g+3 deliver.
-// K and V tiles are stored row-major (16-byte chunks XOR-swizzled by row) in
-// an S-stage LDS ring filled by LDS DMA (global_load_lds_dwordx4: a wave
-// instruction fills 1 KB = 1024 / (2 D) key rows; lane i takes LDS slot i of
-// its row and so reads the chunk that the swizzle puts there), S - 1 tiles in
-// flight while one is used; one barrier per tile.  Registers are capped at
-// 128 per lane (four waves per SIMD) so that two blocks share a CU.
-template <int D, int NW, int S>
-__global__ __launch_bounds__(64 * NW, 4) void attn_prefill_bf16_kernel(PrefillArgs a, float scale_log2) {
-  constexpr int QB = 16 * NW;            // the block's queries (chunk rows)
+// 16-byte chunk swizzle of a K/V row (D / 8 chunks): key row r keeps
+// logical chunk c at c ^ f(r).  For head_dim 128 (256-byte rows, one row
+// per pass over the 64 banks) f is a bijection of r mod 16 that moves
+// aligned groups of four chunks together: 16 consecutive rows read at one
+// chunk (the K operand) land on 16 distinct chunk positions, and the four
+// consecutive rows x four chunks of a transposed V read by 32 lanes land on
+// four distinct groups of four.
+template <int D>
+__device__ __forceinline__ int kv_swz(int c, int r) {
+  if (D == 128) return c ^ (((r & 3) << 2) | ((r >> 2) & 3));
+  return c ^ (r & 7);
+}
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+// One block = one head x (32 * NW queries of the chunk, one range of keys);
+// wave w owns queries w*32 .. w*32+31.  Per 64-key tile:
+//   S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (A = 32 key rows of the K tile,
+//     B = the wave's Q^T fragments held in registers), two 32-key blocks;
+//     lane l holds, per block, the 16 scores of query l % 32 for keys
+//     8*(v/4) + 4*(l/32) + v%4;
+//   the online softmax runs on each query's registers (+1 lane exchange
+//     with lane l ^ 32, which holds the query's other keys);
+//   O^T += V^T P^T (32x32x16: B = the lane's probabilities packed as bf16x8
+//     straight from registers, A = V^T fragments from transposed LDS reads).
+//     The product's k order is a permutation of each 16-key step: lane
+//     group g = l / 32 supplies keys 4g..4g+3 and 8+4g..8+4g+3, which is what
+//     two transposed reads of those four rows deliver.
+// Each LDS byte of K and V feeds 32 queries (twice the 16 of a 16x16 tile).
+// Software pipeline: while the vector ALU runs the softmax of tile k, the
+// matrix cores already compute the scores of tile k + 1 (issued first, no
+// dependency between the two), then O += P V of tile k.  K and V tiles sit
+// in two R-stage LDS rings; iteration k reads K(k + 1) and V(k) and
+// requests V(k + R - 1) and K(k + R) into the stages of V(k - 1) and K(k),
+// so R - 2 tiles of each are in flight while one is used (R = 4: 128 KB
+// for head_dim 128, one block of 8 waves per CU; the depth covers the
+// latency of tiles that come from HBM).  Tiles arrive by LDS DMA
+// (global_load_lds_dwordx4: a wave instruction fills 1 KB = 1024 / (2 D) key
+// rows; lane i takes LDS slot i of its row and so reads the chunk that the
+// swizzle puts there); one barrier per tile.  A wave skips the arithmetic of tiles wholly past its last query
+// (the causal triangle of the chunk).
+// Output: a work item with partial index p >= 0 writes the partial
+// [m, l, o[D]] of each of its rows (merged by the combine pass); p < 0 means
+// the item covers all of its rows' keys, and it writes the normalised rows
+// of O (dtype bf16) directly.
+template <int D, int NW, int R>
+__global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(PrefillArgs a, float scale_log2) {
+  constexpr int QB = 32 * NW;            // the block's queries (chunk rows)
   constexpr int KT = 64;                 // keys per tile
   constexpr int DCH = D / 8;             // 16-byte chunks per K/V row
   constexpr int TILE = KT * DCH;         // 16-byte chunks per K (or V) tile
   constexpr int RPI = 64 / DCH;          // key rows per 1 KB DMA instruction
-  constexpr int GRP = 2 * KT / RPI;      // 1 KB groups per K+V tile pair
-  constexpr int NI = GRP / NW;           // DMA instructions per wave per tile
-  static_assert(NI * NW == GRP && (S - 2) * NI < 64 && S >= 2, "tile DMA split");
-  extern __shared__ u32x4 ring[];        // [S][K tile, V tile]
+  constexpr int NI = KT / RPI / NW;      // DMA instructions per wave per tile (K or V)
+  static_assert(NI * NW * RPI == KT && 2 * (R - 1) * NI < 64 && R >= 3, "tile DMA split");
+  extern __shared__ u32x4 ring[];        // [R] K tiles, then [R] V tiles
+  u32x4* kring = ring;
+  u32x4* vring = ring + R * TILE;
 
   const int per = gridDim.x / 8;
   const int t = (blockIdx.x % 8) * per + blockIdx.x / 8;
@@ -73,7 +136,7 @@ __global__ __launch_bounds__(64 * NW, 4) void attn_prefill_bf16_kernel(PrefillAr
   const int slot = ch[0], offset = ch[1], C = ch[2], row0 = ch[3];
   const int q0 = wk[1] * QB, pslot = wk[2];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int grp = lane >> 4, ql = lane & 15;
+  const int g = lane >> 5, ql = lane & 31;
   const bf16* qkv = reinterpret_cast<const bf16*>(a.qkv) + (size_t)row0 * a.ld_qkv;
   const bf16* cache = reinterpret_cast<const bf16*>(a.kv_layer);
   const bf16* kbase = cache + (size_t)slot * a.st.slot + (size_t)h * a.st.head;
@@ -85,160 +148,333 @@ __global__ __launch_bounds__(64 * NW, 4) void attn_prefill_bf16_kernel(PrefillAr
   const int kend = min(n_keys, (wk[3] & 0xffff) * KT);
   const int n_tiles = (kend - kbeg + KT - 1) / KT;
 
-  // The lane's query (B operand of S^T): q = ql, d = ks*32 + 8*grp.
-  const int myq = q0 + wave * 16 + ql;
+  // The lane's query (B operand of S^T): q = ql, d = ks*16 + 8*g.
+  const int wq0 = q0 + wave * 32;        // the wave's first query
+  const int myq = wq0 + ql;
   const int qpos = offset + myq;
-  u32x4 qf[D / 32];
+  const int last_key = offset + wq0 + 31;   // keys past it are masked for the whole wave
+  u32x4 qf[D / 16];
 #pragma unroll
-  for (int ks = 0; ks < D / 32; ++ks) {
-    const u32x4 v = *reinterpret_cast<const u32x4*>(qkv + (size_t)min(myq, C - 1) * a.ld_qkv + h * D + ks * 32 + 8 * grp);
+  for (int ks = 0; ks < D / 16; ++ks) {
+    const u32x4 v = *reinterpret_cast<const u32x4*>(qkv + (size_t)min(myq, C - 1) * a.ld_qkv + h * D + ks * 16 + 8 * g);
     qf[ks] = (myq < C) ? v : u32x4{0u, 0u, 0u, 0u};
   }
 
   float m_run = -INFINITY, l_run = 0.f;
-  floatx4 o_acc[D / 16];                 // O^T[d = dt*16 + 4*grp + i][q = ql]
+  floatx16 o_acc[D / 32];                // O^T[d = db*32 + 8*(v/4) + 4*g + v%4][q = ql]
 #pragma unroll
-  for (int dt = 0; dt < D / 16; ++dt) o_acc[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) o_acc[db][v] = 0.f;
 
-  // Tile DMA: instruction j of wave w fills 1 KB group g = j * NW + w of the
-  // tile pair (K groups first, then V).  Key addresses are clamped to the
-  // item's last key (finite data; such keys are masked out of the softmax).
+  // Tile DMA: instruction j of wave w fills 1 KB group gi = j * NW + w of a
+  // K or V tile.  Key addresses are clamped to the item's last key (finite
+  // data; such keys are masked out of the softmax).
   const int lrow = lane / DCH, lslot = lane % DCH;
-  const bf16* dsrc[NI];
   int drow[NI];
+  size_t doff[NI];                       // element offset of the lane's 16 bytes in key row drow[j]
 #pragma unroll
   for (int j = 0; j < NI; ++j) {
-    const int g = j * NW + wave;
-    const int kv = g / (KT / RPI), row = (g % (KT / RPI)) * RPI + lrow;
-    drow[j] = row;
-    dsrc[j] = (kv ? vbase : kbase) + (lslot ^ (row & 7)) * 8;
+    drow[j] = (j * NW + wave) * RPI + lrow;
+    doff[j] = (size_t)drow[j] * a.st.pos + kv_swz<D>(lslot, drow[j]) * 8;
   }
-  auto issue = [&](int stage, int kt) {
+  auto issue = [&](const bf16* base, u32x4* stage, int kt) {
     const int k0 = kbeg + kt * KT;
-    uint4* dst = reinterpret_cast<uint4*>(ring + stage * 2 * TILE);
+    uint4* dst = reinterpret_cast<uint4*>(stage);
+    const bf16* tb = base + (size_t)k0 * a.st.pos;
+    if (k0 + KT <= kend) {
 #pragma unroll
-    for (int j = 0; j < NI; ++j)
-      dma16(dsrc[j] + (size_t)min(k0 + drow[j], kend - 1) * a.st.pos, dst + (j * NW + wave) * 64);
+      for (int j = 0; j < NI; ++j) dma16(tb + doff[j], dst + (j * NW + wave) * 64);
+    } else {
+#pragma unroll
+      for (int j = 0; j < NI; ++j) {
+        const int over = max(k0 + drow[j] - (kend - 1), 0);   // rows past the item's last key re-read it
+        dma16(tb + doff[j] - (size_t)over * a.st.pos, dst + (j * NW + wave) * 64);
+      }
+    }
   };
 
-  // Transpose-read addressing of V^T fragments: lane i of group grp reads 8
-  // bytes of row 4*grp + i/4 (+16 for the second half) at columns
-  // dt*16 + 4*(i%4) .. +3.
-  const int tr_row = 4 * grp + (ql >> 2);
-  const int tr_c16 = (ql & 3) >> 1;      // 16-byte chunk within the 16 columns of dt
-  const int tr_half = (ql & 1) * 8;      // byte offset inside the chunk
-
+  // Transposed-read addressing of V^T fragments: within its 16-lane group
+  // G = lane / 16, lane i = 4e + q reads 8 bytes of key row 8h + 4g + e
+  // (+16 per key step) at columns db*32 + 16*(G % 2) + 4q .. +3.
+  // The swizzle depends on the row only through its index mod 16, so each
+  // lane's byte offsets are fixed for the whole loop: the 16-key steps and
+  // 32-key blocks add constants (the LDS reads' immediate offsets).
+  const int G = lane >> 4, li = lane & 15;
+  const int tr_e = li >> 2, tr_q = li & 3;
+  const int tr_c16 = 2 * (G & 1) + (tr_q >> 1);   // 16-byte chunk within the 32 columns of db
+  const int tr_half = (tr_q & 1) * 8;              // byte offset inside the chunk
+  int voff[2][D / 32];                             // rows 4g + tr_e (+8) of a V tile
 #pragma unroll
-  for (int st = 0; st < S - 1; ++st)
-    if (st < n_tiles) issue(st, st);
-  int buf = 0, nbuf = S - 1;
-  for (int kt = 0; kt < n_tiles; ++kt) {
-    const int k0 = kbeg + kt * KT;
-    if (kt + S - 2 < n_tiles) wait_vmcnt<(S - 2) * NI>();
-    else wait_vmcnt<0>();
-    lds_read_barrier();
-    if (kt + S - 1 < n_tiles) issue(nbuf, kt + S - 1);
-    const u32x4* ks_ = ring + buf * 2 * TILE;
-    const u32x4* vs_ = ks_ + TILE;
-    buf = (buf + 1 == S) ? 0 : buf + 1;
-    nbuf = (nbuf + 1 == S) ? 0 : nbuf + 1;
-
-    // ---- S^T = K Q^T: s[nt][i] = score of key k0 + nt*16 + 4*grp + i for query ql.
-    floatx4 s[KT / 16];
+  for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-    for (int nt = 0; nt < KT / 16; ++nt) {
-      s[nt] = floatx4{0.f, 0.f, 0.f, 0.f};
-      const int key = nt * 16 + ql;
-#pragma unroll
-      for (int ks = 0; ks < D / 32; ++ks) {
-        const int ch = ks * 4 + grp;
-        const bf16x8_t kf = __builtin_bit_cast(bf16x8_t, ks_[key * DCH + (ch ^ (key & 7))]);
-        s[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, __builtin_bit_cast(bf16x8_t, qf[ks]), s[nt], 0, 0, 0);
-      }
+    for (int db = 0; db < D / 32; ++db) {
+      const int r = 4 * g + tr_e + 8 * hh;
+      voff[hh][db] = (r * DCH + kv_swz<D>(4 * db + tr_c16, r)) * 16 + tr_half;
     }
+  int koff[D / 16];                                // row ql of a K tile, chunk 2 ks + g
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) koff[ks] = (ql * DCH + kv_swz<D>(2 * ks + g, ql)) * 16;
 
-    // ---- online softmax (log2 units).  Keys past the query's position or the
-    // item's end are masked; a tile entirely before every query of the wave
-    // and inside the item needs no mask.
-    const bool full = k0 + KT <= kend && k0 + KT - 1 <= offset + q0 + wave * 16;
+  // scores of one tile: s[kb][v] = score of key k0 + kb*32 + 8*(v/4) + 4*g + v%4 for query ql
+  auto scores = [&](const u32x4* ks_, floatx16* s) {
+    const uint32_t kb_ = lds_addr(ks_);
+    u32x4 kf[2][D / 16];
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) kf[0][ks] = lds_b128_asm<0>(kb_ + koff[ks]);
+    lds_wait(kf[0]);
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) kf[1][ks] = lds_b128_asm<32 * DCH * 16>(kb_ + koff[ks]);
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      if (kb == 1) lds_wait(kf[1]);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) s[kb][v] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < D / 16; ++ks)
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kf[kb][ks]),
+                                                        __builtin_bit_cast(bf16x8_t, qf[ks]), s[kb], 0, 0, 0);
+    }
+  };
+
+  const int n = n_tiles;
+  floatx16 s_cur[2], s_next[2];
+  // Requests come in batches, batch j = {V(j + R - 1), K(j + R)} (tiles past
+  // the item's end are skipped); iteration k needs K(k + 1) and V(k), both
+  // of batch k - R + 1, so the batches after it may stay in flight: the LDS
+  // DMA of a wave completes in issue order.  in_flight(k) counts those
+  // instructions (V tiles k + 1 .. k + R - 2, K tiles k + 2 .. k + R - 1).
+  auto cnt = [&](int lo, int hi) { return max(0, min(hi, n - 1) - lo + 1); };   // tiles in [lo, hi] below n
+  auto wait_in_flight = [&](int c) {          // c: instructions that may remain outstanding
+    switch (c / NI) {
+      case 0: wait_vmcnt<0>(); break;
+      case 1: wait_vmcnt<NI>(); break;
+      case 2: wait_vmcnt<2 * NI>(); break;
+      case 3: wait_vmcnt<3 * NI>(); break;
+      case 4: wait_vmcnt<4 * NI>(); break;
+      case 5: wait_vmcnt<5 * NI>(); break;
+      case 6: wait_vmcnt<6 * NI>(); break;
+      case 7: wait_vmcnt<7 * NI>(); break;
+      default: wait_vmcnt<8 * NI>(); break;
+    }
+  };
+  static_assert(2 * (R - 1) <= 8 && 8 * NI < 64, "wait cases");
+  // prologue: K(0), then batches 1 - R .. -1 = V(0 .. R - 2), K(1 .. R - 1);
+  // scores of tile 0 once K(0) has landed
+  issue(kbase, kring, 0);
+  for (int j = 0; j < R - 1; ++j) {
+    if (j < n) issue(vbase, vring + j * TILE, j);
+    if (j + 1 < n) issue(kbase, kring + (j + 1) * TILE, j + 1);
+  }
+  wait_in_flight(NI * (cnt(0, R - 2) + cnt(1, R - 1)));
+  lds_read_barrier();
+  if (kbeg <= last_key) scores(kring, s_cur);
+
+  // One tile: scores of tile kt are in sc; the scores of tile kt + 1 go to sn.
+  auto step = [&](int kt, floatx16* sc, floatx16* sn) {
+    const int k0 = kbeg + kt * KT;
+    // K(kt + 1) and V(kt) have landed; after the barrier every wave is done
+    // with K(kt) and V(kt - 1), whose stages take V(kt + R - 1) and K(kt + R)
+    wait_in_flight(NI * (cnt(kt + 1, kt + R - 2) + cnt(kt + 2, kt + R - 1)));
+    lds_read_barrier();
+    if (kt + R - 1 < n) issue(vbase, vring + ((kt + R - 1) % R) * TILE, kt + R - 1);
+    if (kt + R < n) issue(kbase, kring + (kt % R) * TILE, kt + R);
+    // every key of the tile lies past the wave's last query: nothing to add
+    // (and none of the later tiles adds anything either)
+    if (k0 > last_key) return;
+    // the K fragments of tile kt + 1 are requested first: they arrive while
+    // the vector ALU masks and takes the maximum of tile kt (the K stage of
+    // tile kt + 1 exists in every iteration; past the item's end its stale
+    // values are computed on and never used)
+    const uint32_t kn = lds_addr(kring + ((kt + 1) % R) * TILE);
+    u32x4 kf[2][D / 16];
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) kf[0][ks] = lds_b128_asm<0>(kn + koff[ks]);
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) kf[1][ks] = lds_b128_asm<32 * DCH * 16>(kn + koff[ks]);
+
+    // ---- keys past the query's position or the item's end are masked; a
+    // tile wholly before every query of the wave and inside the item needs
+    // no mask
+    const bool full = k0 + KT <= kend && k0 + KT - 1 <= offset + wq0;
     if (!full) {
 #pragma unroll
-      for (int nt = 0; nt < KT / 16; ++nt)
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int kp = k0 + nt * 16 + 4 * grp + i;
-          if (!(kp <= qpos && kp < kend)) s[nt][i] = -INFINITY;
+        for (int v = 0; v < 16; ++v) {
+          const int kp = k0 + kb * 32 + 8 * (v >> 2) + 4 * g + (v & 3);
+          if (!(kp <= qpos && kp < kend)) sc[kb][v] = -INFINITY;
         }
     }
+    // ---- running max, moved only when a tile's max exceeds it by more than
+    // 2^8 (the probabilities of a tile stay below 256: fp32 sums and bf16
+    // products keep their relative precision; O and l are rescaled together)
     float mx = -INFINITY;
 #pragma unroll
-    for (int nt = 0; nt < KT / 16; ++nt)
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[nt][i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx * scale_log2);
-    const float m_safe = (m_new == -INFINITY) ? 0.f : m_new;
-    const float corr = __builtin_amdgcn_exp2f(m_run - m_safe);
-    float sum = 0.f;
+      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sc[kb][v]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * scale_log2;
+    if (__ballot(mx > m_run + 8.0f)) {
+      const float m_new = fmaxf(m_run, mx);
+      // 0 while m_run is -inf; a lane whose keys are all masked so far keeps 1
+      const float corr = (m_new == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f(m_run - m_new);
 #pragma unroll
-    for (int nt = 0; nt < KT / 16; ++nt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        s[nt][i] = __builtin_amdgcn_exp2f(fmaf(s[nt][i], scale_log2, -m_safe));
-        sum += s[nt][i];
-      }
-    sum += __shfl_xor(sum, 16, 64);
-    sum += __shfl_xor(sum, 32, 64);
-    l_run = l_run * corr + sum;
-    m_run = m_new;
-    if (__ballot(corr != 1.0f)) {
-#pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) o_acc[dt] *= corr;
+      for (int db = 0; db < D / 32; ++db) o_acc[db] *= corr;
+      l_run *= corr;
+      m_run = m_new;
     }
+    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
 
-    // ---- O^T += V^T P^T over two 32-key blocks.
-    const char* vb = reinterpret_cast<const char*>(vs_);
+    // ---- the scores of tile kt + 1 on the matrix cores, interleaved with the
+    // exponentials of tile kt on the vector ALU
+    float sum = 0.f;
+    u32x4 pw[4];
+    lds_wait(kf[0]);
+    lds_wait(kf[1]);
 #pragma unroll
-    for (int kk = 0; kk < KT / 32; ++kk) {
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) sn[kb][v] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < D / 16; ++ks)
+        sn[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kf[kb][ks]),
+                                                         __builtin_bit_cast(bf16x8_t, qf[ks]), sn[kb], 0, 0, 0);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        sc[kb][v] = __builtin_amdgcn_exp2f(fmaf(sc[kb][v], scale_log2, -m_use));
+        sum += sc[kb][v];
+      }
       // probabilities to bf16 (round to nearest even, v_cvt_pk_bf16_f32)
-      const u32x4 pw{pack_bf16x2(s[2 * kk][0], s[2 * kk][1]), pack_bf16x2(s[2 * kk][2], s[2 * kk][3]),
-                     pack_bf16x2(s[2 * kk + 1][0], s[2 * kk + 1][1]), pack_bf16x2(s[2 * kk + 1][2], s[2 * kk + 1][3])};
-      const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, pw);
-      const int r0 = kk * 32 + tr_row, r1 = r0 + 16;
 #pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) {
-        const int c16 = 2 * dt + tr_c16;
-        const uint2 lo = lds_read_tr16(vb + (r0 * DCH + (c16 ^ (r0 & 7))) * 16 + tr_half);
-        const uint2 hi = lds_read_tr16(vb + (r1 * DCH + (c16 ^ (r1 & 7))) * 16 + tr_half);
-        const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, u32x4{lo.x, lo.y, hi.x, hi.y});
-        o_acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o_acc[dt], 0, 0, 0);
+      for (int h2 = 0; h2 < 2; ++h2) {
+        const int vo = h2 * 8;
+        pw[2 * kb + h2] = u32x4{pack_bf16x2(sc[kb][vo], sc[kb][vo + 1]), pack_bf16x2(sc[kb][vo + 2], sc[kb][vo + 3]),
+                                pack_bf16x2(sc[kb][vo + 4], sc[kb][vo + 5]), pack_bf16x2(sc[kb][vo + 6], sc[kb][vo + 7])};
+      }
+      // one matrix product, then about five vector instructions, in turn
+#pragma unroll
+      for (int i = 0; i < D / 16; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
       }
     }
+    sum += __shfl_xor(sum, 32, 64);
+    l_run += sum;
+
+    // ---- O^T += V^T P^T over four 16-key steps; the V fragments of a step
+    // are read while the previous step's products run.
+    const uint32_t vb = lds_addr(vring + (kt % R) * TILE);
+    uint32_t va[2][D / 32];
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) va[hh][db] = vb + voff[hh][db];
+    constexpr int STEP = 16 * DCH * 16;   // bytes of 16 key rows
+    auto vread = [&](u32x2* vr, int ks2) {
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) {
+        switch (ks2) {
+          case 0: vr[2 * db] = lds_tr16_asm<0>(va[0][db]); vr[2 * db + 1] = lds_tr16_asm<0>(va[1][db]); break;
+          case 1: vr[2 * db] = lds_tr16_asm<STEP>(va[0][db]); vr[2 * db + 1] = lds_tr16_asm<STEP>(va[1][db]); break;
+          case 2: vr[2 * db] = lds_tr16_asm<2 * STEP>(va[0][db]); vr[2 * db + 1] = lds_tr16_asm<2 * STEP>(va[1][db]); break;
+          default: vr[2 * db] = lds_tr16_asm<3 * STEP>(va[0][db]); vr[2 * db + 1] = lds_tr16_asm<3 * STEP>(va[1][db]); break;
+        }
+      }
+    };
+    u32x2 vr[2][2 * (D / 32)];
+    vread(vr[0], 0);
+#pragma unroll
+    for (int ks2 = 0; ks2 < KT / 16; ++ks2) {
+      // the next step's V fragments are requested before this step's products
+      if (ks2 + 1 < KT / 16) {
+        vread(vr[(ks2 + 1) & 1], ks2 + 1);
+        lds_wait_but<2 * (D / 32)>(vr[ks2 & 1]);   // the next step's reads may stay in flight
+      } else {
+        lds_wait(vr[ks2 & 1]);
+      }
+      const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, pw[ks2]);
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) {
+        const u32x2* vc = vr[ks2 & 1];
+        const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, u32x4{vc[2 * db].x, vc[2 * db].y, vc[2 * db + 1].x,
+                                                               vc[2 * db + 1].y});
+        o_acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, o_acc[db], 0, 0, 0);
+      }
+    }
+  };
+
+  // two tiles per trip, the score buffers alternating
+  for (int kt = 0; kt < n; kt += 2) {
+    step(kt, s_cur, s_next);
+    if (kt + 1 < n) step(kt + 1, s_next, s_cur);
   }
 
-  // ---- partial of the lane's query (rows < C): [m, l, o[D]].
-  const int rb = wave * 16 + ql;
-  if (q0 + rb < C) {
-    float* dst = a.part + ((size_t)(pslot * QB + rb) * a.nh + h) * (D + 2);
-    if (grp == 0) {
-      dst[0] = m_run;
-      dst[1] = l_run;
+  // ---- epilogue.  The lane holds column block d of query ql; rows of O (or
+  // of the partial) are contiguous in memory, so each wave first transposes
+  // its 32 x D tile through LDS (16-byte chunks XOR-swizzled by row), then
+  // writes whole rows, 16 bytes per lane.  The K/V rings are free once every
+  // wave has passed the barrier.
+  lds_read_barrier();
+  const int nrows = min(32, C - wq0);     // the wave's rows inside the chunk
+  if (pslot < 0) {
+    // the item saw every key of its rows: normalised O in the output dtype
+    constexpr int RC = D / 8;             // 16-byte chunks per bf16 row
+    char* T = reinterpret_cast<char*>(ring) + wave * 32 * D * 2;
+    const float inv = 1.0f / l_run;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int v4 = 0; v4 < 4; ++v4) {
+        const uint2 w{pack_bf16x2(o_acc[db][4 * v4] * inv, o_acc[db][4 * v4 + 1] * inv),
+                      pack_bf16x2(o_acc[db][4 * v4 + 2] * inv, o_acc[db][4 * v4 + 3] * inv)};
+        const int c = db * 4 + v4;        // 16-byte chunk of columns db*32 + 8*v4 .. +7
+        *reinterpret_cast<uint2*>(T + ql * D * 2 + (c ^ (ql & (RC - 1))) * 16 + g * 8) = w;
+      }
+    __builtin_amdgcn_s_waitcnt(0xc07f);   // this wave's LDS writes done (lgkmcnt 0)
+#pragma unroll
+    for (int i = 0; i < 32 * RC / 64; ++i) {
+      const int idx = i * 64 + lane, r = idx / RC, c = idx % RC;
+      const u32x4 v = *reinterpret_cast<const u32x4*>(T + r * D * 2 + (c ^ (r & (RC - 1))) * 16);
+      if (r < nrows)
+        *reinterpret_cast<u32x4*>(reinterpret_cast<bf16*>(a.out) + (size_t)(row0 + wq0 + r) * a.ld_out + h * D +
+                                  c * 8) = v;
     }
+    return;
+  }
+  // partial of each row: [m, l, -, -, o[D]]
+  constexpr int RC = D / 4;               // 16-byte chunks per fp32 row
+  float* T = reinterpret_cast<float*>(ring) + wave * 32 * D;
 #pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt)
+  for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) dst[2 + dt * 16 + 4 * grp + i] = o_acc[dt][i];
+    for (int v4 = 0; v4 < 4; ++v4) {
+      const int c = db * 8 + 2 * v4 + g;  // 16-byte chunk of columns db*32 + 8*v4 + 4*g .. +3
+      *reinterpret_cast<floatx4*>(T + ql * D + (c ^ (ql & 15)) * 4) =
+          floatx4{o_acc[db][4 * v4], o_acc[db][4 * v4 + 1], o_acc[db][4 * v4 + 2], o_acc[db][4 * v4 + 3]};
+    }
+  float* prow = a.part + (size_t)(pslot * QB + wave * 32) * a.nh * (D + PART_O) + (size_t)h * (D + PART_O);
+  const size_t rstride = (size_t)a.nh * (D + PART_O);
+  if (g == 0 && ql < nrows) {
+    prow[ql * rstride] = m_run;
+    prow[ql * rstride + 1] = l_run;
+  }
+  __builtin_amdgcn_s_waitcnt(0xc07f);     // this wave's LDS writes done (lgkmcnt 0)
+#pragma unroll
+  for (int i = 0; i < 32 * RC / 64; ++i) {
+    const int idx = i * 64 + lane, r = idx / RC, c = idx % RC;
+    const floatx4 v = *reinterpret_cast<const floatx4*>(T + r * D + (c ^ (r & 15)) * 4);
+    if (r < nrows) *reinterpret_cast<floatx4*>(prow + r * rstride + PART_O + c * 4) = v;
   }
 }
 
-template <int D, int NW, int S>
+template <int D, int NW, int R>
 static hipError_t run_prefill(const PrefillArgs& a, unsigned grid, float scale_log2, hipStream_t s) {
-  const size_t lds_bytes = (size_t)S * 2 * 64 * (D / 8) * 16;
+  const size_t lds_bytes = (size_t)2 * R * 64 * (D / 8) * 16;   // R K + R V tile stages
   static std::atomic<uint64_t> lds_set{0};   // devices on which this instance's LDS limit is raised
-  hipError_t e = ensure_dynamic_lds((const void*)attn_prefill_bf16_kernel<D, NW, S>, (int)lds_bytes, lds_set);
+  hipError_t e = ensure_dynamic_lds((const void*)attn_prefill_bf16_kernel<D, NW, R>, (int)lds_bytes, lds_set);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attn_prefill_bf16_kernel<D, NW, S>), dim3(grid), dim3(64 * NW), lds_bytes, s, a, scale_log2);
+  hipLaunchKernelGGL((attn_prefill_bf16_kernel<D, NW, R>), dim3(grid), dim3(64 * NW), lds_bytes, s, a, scale_log2);
   return hipGetLastError();
 }
 
@@ -247,10 +483,10 @@ hipError_t launch_attn_prefill(int dtype, const PrefillArgs& a, hipStream_t s) {
   if (dtype != 1) return hipErrorInvalidValue;
   const float scale_log2 = LOG2E / sqrtf((float)a.hd);
   const unsigned grid = (unsigned)(((size_t)a.n_work * a.nh + 7) / 8 * 8);
-  constexpr int NW = PREFILL_QBLOCK / 16;
-  // two stages (64 KB for head_dim 128): two blocks per CU
-  if (a.hd == 128) return run_prefill<128, NW, 2>(a, grid, scale_log2, s);
-  return run_prefill<64, NW, 2>(a, grid, scale_log2, s);
+  constexpr int NW = PREFILL_QBLOCK / 32;
+  // 4-deep K and V rings: 128 KB for head_dim 128, one block of 8 waves per CU
+  if (a.hd == 128) return run_prefill<128, NW, 4>(a, grid, scale_log2, s);
+  return run_prefill<64, NW, 4>(a, grid, scale_log2, s);
 }
 
 }  // namespace sarathi

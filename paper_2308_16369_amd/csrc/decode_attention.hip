@@ -146,12 +146,12 @@ __global__ __launch_bounds__(256) void attn_rows_kernel(RowAttnArgs a, float sca
   __syncthreads();
   float M = fmaxf(fmaxf(red_m[0], red_m[1]), fmaxf(red_m[2], red_m[3]));
   const float Ms = (M == -INFINITY) ? 0.f : M;
-  float* dst = a.part + ((size_t)(a.part_base + item) * a.nh + h) * (D + 2);
+  float* dst = a.part + ((size_t)(a.part_base + item) * a.nh + h) * (D + PART_O);
   for (int d = tid; d < D; d += 256) {
     float acc = 0.f;
 #pragma unroll
     for (int w = 0; w < 4; ++w) acc += red_o[w][d] * exp2f(red_m[w] - Ms);
-    dst[2 + d] = acc;
+    dst[PART_O + d] = acc;
   }
   if (tid == 0) {
     float L = 0.f;
@@ -362,12 +362,12 @@ __global__ __launch_bounds__(64 * NWV) void attn_rows_bf16_kernel(RowAttnArgs a,
 #pragma unroll
   for (int w = 1; w < NWV; ++w) Mb = fmaxf(Mb, red_m[w]);
   const float Ms = (Mb == -INFINITY) ? 0.f : Mb;
-  float* dst = a.part + ((size_t)(a.part_base + item) * a.nh + h) * (D + 2);
+  float* dst = a.part + ((size_t)(a.part_base + item) * a.nh + h) * (D + PART_O);
   for (int d = tid; d < D; d += 64 * NWV) {
     float acc = 0.f;
 #pragma unroll
     for (int w = 0; w < NWV; ++w) acc += red_o[w][d] * exp2f(red_m[w] - Ms);
-    dst[2 + d] = acc;
+    dst[PART_O + d] = acc;
   }
   if (tid == 0) {
     float Lb = 0.f;

@@ -91,10 +91,12 @@ int linear_tile_count();
 bool linear_tile_shape(int tile, int* bm, int* bn);
 
 // ---- attention
-// Partial results (one per row x head x key split): [m, l, o[hd]] in fp32,
-// m the running max of the log2-scaled scores, l the sum of 2^(s - m),
-// o the unnormalised weighted sum of values.
-constexpr int PREFILL_QBLOCK = 128;   // chunk rows per chunk-attention work item
+// Partial results (one per row x head x key split): [m, l, -, -, o[hd]] in
+// fp32 (hd + PART_O floats, so o starts 16-byte aligned), m the running max
+// of the log2-scaled scores, l the sum of 2^(s - m), o the unnormalised
+// weighted sum of values.
+constexpr int PART_O = 4;
+constexpr int PREFILL_QBLOCK = 256;   // chunk rows per chunk-attention work item (8 waves x 32)
 struct PrefillArgs {
   const void* qkv;      // all rows; chunk c's rows start at its first-row entry; q columns rotated
   int ld_qkv;
@@ -105,6 +107,8 @@ struct PrefillArgs {
   const int* work;      // [n_work][chunk, q_block, partial slot p, (first key tile << 16) | end key tile]
   int n_work;
   float* part;          // row j of an item's q-block -> partial index p * PREFILL_QBLOCK + j
+  void* out;            // p < 0 (the item covers every key of its rows): normalised rows of O [T, nh*hd]
+  int ld_out;
 };
 hipError_t launch_attn_prefill(int dtype, const PrefillArgs& a, hipStream_t s);
 
@@ -124,11 +128,13 @@ struct RowAttnArgs {
 };
 hipError_t launch_attn_rows(int dtype, const RowAttnArgs& a, hipStream_t s);
 
-// Combine: row r's partials are comb[3r] + j * comb[3r + 2] for j < comb[3r + 1].
+// Combine: row r's partials are comb[3r] + j * comb[3r + 2] for j < comb[3r + 1];
+// rows with no partials (comb[3r + 1] == 0: written by their attention kernel)
+// are left alone.  Rows row0 .. n_rows - 1 are visited.
 struct CombineArgs {
   const float* part;
   const int* comb;
-  int n_rows, nh, hd;
+  int row0, n_rows, nh, hd;
   void* out;            // [n_rows, nh * hd]
   int ld_out;
 };

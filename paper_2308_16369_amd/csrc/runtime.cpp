@@ -109,7 +109,7 @@ Layout make_layout(const sarathi_model_cfg* c, int T, int n_chunks, int S) {
   // key range per PRE_SPLIT keys each
   const size_t max_pre = ((size_t)(T + QBLOCK - 1) / QBLOCK + n_chunks - 1) * ((S + PRE_SPLIT - 1) / PRE_SPLIT);
   const size_t max_dec = (size_t)T * ((S + SPLIT_KEYS - 1) / SPLIT_KEYS);
-  L.part = take((max_pre * QBLOCK + max_dec) * c->n_heads * (c->head_dim + 2) * 4);
+  L.part = take((max_pre * QBLOCK + max_dec) * c->n_heads * (c->head_dim + PART_O) * 4);
   L.meta = take(((size_t)T * 5 + (size_t)n_chunks * 4 + max_pre * 4 + max_dec) * 4);
   L.ping0 = take(T * H * es);
   L.ping1 = take(T * H * es);
@@ -166,6 +166,8 @@ int from_mixed(const sarathi_mixed_batch* b, BatchDesc* out) {
 // Host-side description of the batch and its device metadata.
 struct Plan {
   int C, B, T, row_base, n_pre, n_dec, n_chunks, pre_tiles;
+  int pre_slots;   // partial q-block slots of the chunk items (items covering all keys of their rows write O)
+  int comb_row0;   // first row whose attention output the combine pass writes
   // row_slot[T] row_pos[T] comb[3T] chunk table [n_chunks][slot, offset, len, first row]
   // pre_work[n_pre][chunk, q_block, partial slot, (first tile << 16) | end tile] dec_work[n_dec]
   std::vector<int> meta;
@@ -216,6 +218,7 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
   // row at position p is attention over keys 0..p, like a decode with ctx = p).
   p.row_base = (cfg->dtype == SARATHI_BF16) ? p.C : 0;
   p.pre_tiles = PRE_SPLIT / 64;
+  p.pre_slots = 0;
   std::vector<int> slot(p.T), pos(p.T), comb(3 * p.T), tab, pre, dec;
   int r0 = 0;
   for (const ChunkDesc& c : b.chunks) {
@@ -231,7 +234,7 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
     // XCD's L2, see the chunk-attention kernel).
     // Key ranges: each q-block's keys, in 64-key tiles, are cut into ns
     // near-equal ranges of at most tau tiles (tau >= PRE_SPLIT / 64).  tau
-    // minimises rounds of blocks (two per CU) x (largest range + ~4 tiles of
+    // minimises rounds of blocks (one per CU) x (largest range + ~4 tiles of
     // fixed cost per block), fitted to measurements of the LLaMA-33B and
     // GPT-3 chunk shapes; ties go to the larger tau (fewer partials).
     std::vector<int> qtiles;   // tiles of every q-block, chunk by chunk
@@ -254,7 +257,7 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
         longest = std::max(longest, (t + ns - 1) / ns);
       }
       blocks *= cfg->n_heads;
-      const double cost = (double)((blocks + 511) / 512) * (longest + 4);
+      const double cost = (double)((blocks + 255) / 256) * (longest + 4);
       if (cost <= best) {
         best = cost;
         tau = cand;
@@ -263,6 +266,9 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
     p.pre_tiles = tau;
     r0 = 0;
     int slot_base = 0, qi = 0;
+    // a q-block whose keys form one range is one item that writes its rows
+    // of O directly (partial slot -1, no combine); split q-blocks get
+    // consecutive partial slots
     for (int ci = 0; ci < p.n_chunks; ++ci) {
       const ChunkDesc& c = b.chunks[ci];
       const int nqb = (c.len + QBLOCK - 1) / QBLOCK;
@@ -271,12 +277,12 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
       for (int qb = 0; qb < nqb; ++qb) {
         nt[qb] = qtiles[qi++];
         ns[qb] = (nt[qb] + tau - 1) / tau;
-        first[qb] = slot_base;
-        slot_base += ns[qb];
+        first[qb] = ns[qb] > 1 ? slot_base : -1;
+        if (ns[qb] > 1) slot_base += ns[qb];
         max_ns = std::max(max_ns, ns[qb]);
         for (int r = qb * QBLOCK; r < std::min((qb + 1) * QBLOCK, c.len); ++r) {
-          comb[3 * (r0 + r)] = first[qb] * QBLOCK + (r - qb * QBLOCK);
-          comb[3 * (r0 + r) + 1] = ns[qb];
+          comb[3 * (r0 + r)] = ns[qb] > 1 ? first[qb] * QBLOCK + (r - qb * QBLOCK) : 0;
+          comb[3 * (r0 + r) + 1] = ns[qb] > 1 ? ns[qb] : 0;
           comb[3 * (r0 + r) + 2] = QBLOCK;
         }
       }
@@ -284,12 +290,13 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
         for (int qb = 0; qb < nqb; ++qb)
           if (s < ns[qb]) {
             const int t0 = (int)((long)nt[qb] * s / ns[qb]), t1 = (int)((long)nt[qb] * (s + 1) / ns[qb]);
-            pre.insert(pre.end(), {ci, qb, first[qb] + s, (t0 << 16) | t1});
+            pre.insert(pre.end(), {ci, qb, ns[qb] > 1 ? first[qb] + s : -1, (t0 << 16) | t1});
           }
       r0 += c.len;
     }
+    p.pre_slots = slot_base;
   }
-  const int pre_rows = (int)pre.size() / 4 * QBLOCK;
+  const int pre_rows = p.pre_slots * QBLOCK;
   // Row-attention items run in the order of the rows' KV slots (each row's
   // splits together), so the blocks in flight stream the cache in address
   // order (measured ~2% faster than a random slot order).
@@ -305,6 +312,12 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
   }
   p.n_pre = (int)pre.size() / 4;
   p.n_dec = (int)dec.size();
+  p.comb_row0 = p.T;
+  for (int r = 0; r < p.T; ++r)
+    if (comb[3 * r + 1] > 0) {
+      p.comb_row0 = r;
+      break;
+    }
   p.meta.reserve(5 * p.T + tab.size() + pre.size() + dec.size());
   p.o_slot = 0; p.meta.insert(p.meta.end(), slot.begin(), slot.end());
   p.o_pos = p.meta.size(); p.meta.insert(p.meta.end(), pos.begin(), pos.end());
@@ -443,6 +456,7 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
     pa.qkv = ws + c.L.qkv; pa.ld_qkv = 3 * QD; pa.kv_layer = kv_layer; pa.st = c.kv->st;
     pa.chunks = meta + P.o_chunks; pa.nh = nh; pa.hd = hd;
     pa.work = meta + P.o_pre; pa.n_work = P.n_pre; pa.part = part;
+    pa.out = ws + c.L.o; pa.ld_out = QD;
     e = launch_attn_prefill(dt, pa, c.s);
     if (e != hipSuccess) return hip_fail(e, "chunk attention");
   }
@@ -452,13 +466,14 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
     da.qkv = ws + c.L.qkv; da.ld_qkv = 3 * QD; da.kv_layer = kv_layer; da.st = c.kv->st;
     da.row_slot = meta + P.o_slot; da.row_pos = meta + P.o_pos; da.work = meta + P.o_dec;
     da.row_base = P.row_base; da.n_work = P.n_dec; da.split_keys = SPLIT_KEYS; da.nh = nh; da.hd = hd;
-    da.part = part; da.part_base = P.n_pre * QBLOCK;
+    da.part = part; da.part_base = P.pre_slots * QBLOCK;
     e = launch_attn_rows(dt, da, c.s);
     if (e != hipSuccess) return hip_fail(e, "decode attention");
   }
   SARATHI_MARK();
   CombineArgs ca{};
-  ca.part = part; ca.comb = meta + P.o_comb; ca.n_rows = T; ca.nh = nh; ca.hd = hd; ca.out = ws + c.L.o;
+  ca.part = part; ca.comb = meta + P.o_comb; ca.row0 = P.comb_row0; ca.n_rows = T; ca.nh = nh; ca.hd = hd;
+  ca.out = ws + c.L.o;
   ca.ld_out = QD;
   e = launch_attn_combine(dt, ca, c.s);
   if (e != hipSuccess) return hip_fail(e, "attention combine");
@@ -542,8 +557,8 @@ int prepare(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, int n_
   *plan = make_plan(cfg, batch);
   // the plan must fit the regions the layout sized for it (an internal
   // invariant: the bounds above hold for every batch check_batch accepts)
-  const size_t part_rows = (L->meta - L->part) / ((size_t)cfg->n_heads * (cfg->head_dim + 2) * 4);
-  if (plan->meta.size() * 4 > L->ping0 - L->meta || (size_t)plan->n_pre * QBLOCK + plan->n_dec > part_rows)
+  const size_t part_rows = (L->meta - L->part) / ((size_t)cfg->n_heads * (cfg->head_dim + PART_O) * 4);
+  if (plan->meta.size() * 4 > L->ping0 - L->meta || (size_t)plan->pre_slots * QBLOCK + plan->n_dec > part_rows)
     return fail(SARATHI_EINVAL, "internal: batch plan exceeds its workspace layout");
   return SARATHI_OK;
 }
@@ -786,6 +801,38 @@ int linear_common(int dtype, int kind, int M, int N, int K, const void* x, const
 int sarathi_linear(int dtype, int kind, int M, int N, int K, const void* x, const void* w, const void* resid,
                    void* out, void* scratch, size_t scratch_bytes, void* hip_stream) {
   return linear_common(dtype, kind, M, N, K, x, w, resid, out, scratch, scratch_bytes, hip_stream, -1, 0);
+}
+
+int sarathi_attention_plan(const sarathi_model_cfg* cfg, const sarathi_hybrid_batch* batch, sarathi_attn_plan* out) {
+  if (!out) return fail(SARATHI_EINVAL, "out is NULL");
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  BatchDesc b;
+  rc = from_hybrid(batch, &b);
+  if (rc) return rc;
+  if (b.rows() < 1) return fail(SARATHI_EINVAL, "empty batch (no chunk rows and no decodes)");
+  if (b.B > 0 && (!b.dslots || !b.dctx)) return fail(SARATHI_EINVAL, "decode arrays are NULL");
+  const Plan P = make_plan(cfg, b);
+  const int* comb = P.meta.data() + P.o_comb;
+  const int* pre = P.meta.data() + P.o_pre;
+  const int* chunks = P.meta.data() + P.o_chunks;
+  sarathi_attn_plan o{};
+  o.chunk_items = P.n_pre;
+  o.decode_items = P.n_dec;
+  long written = P.n_dec;
+  for (int i = 0; i < P.n_pre; ++i)
+    if (pre[4 * i + 2] >= 0) {
+      const int len = chunks[4 * pre[4 * i] + 2], q0 = pre[4 * i + 1] * QBLOCK;
+      written += std::min(QBLOCK, len - q0);
+    }
+  o.partial_rows_written = written;
+  for (int r = 0; r < P.T; ++r)
+    if (comb[3 * r + 1] > 0) {
+      o.partial_rows_read += comb[3 * r + 1];
+      ++o.combine_rows;
+    }
+  *out = o;
+  return SARATHI_OK;
 }
 
 int sarathi_linear_plan(int dtype, int kind, int M, int N, int K, size_t scratch_bytes, int* bm, int* bn,

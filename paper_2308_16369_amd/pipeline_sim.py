@@ -114,10 +114,12 @@ def measure_cost_model(shape, max_seq: int = 4096, max_decodes: int = 32, log=la
     def stages(calls, iters=4):
         return r.stages(calls, iters)
 
+    for T in grid:   # one untimed pass first: the first launch of each kernel instance is not its cost
+        r.call(Batch(0, 0, T, [], []))()
     lin = []
-    for T in grid:   # prefill-only at offset 0: non-attention stages
-        st = stages([r.call(Batch(0, 0, T, [], []))])
-        lin.append(sum(st[k] for k in NON_ATTN))
+    for T in grid:   # prefill-only at offset 0: non-attention stages (median of three)
+        reps = [sum(stages([r.call(Batch(0, 0, T, [], []))])[k] for k in NON_ATTN) for _ in range(3)]
+        lin.append(float(np.median(reps)))
     log("linear table measured")
     Xp, yp = [], []
     for off in sorted({0, 256, 1024, 2048, max(0, max_seq - 512)}):

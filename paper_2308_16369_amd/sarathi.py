@@ -71,6 +71,11 @@ class sarathi_ws_layout(ct.Structure):
                                                                              ("total", ct.c_size_t)]
 
 
+class sarathi_attn_plan(ct.Structure):
+    _fields_ = [("chunk_items", ct.c_int), ("decode_items", ct.c_int), ("partial_rows_written", ct.c_long),
+                ("partial_rows_read", ct.c_long), ("combine_rows", ct.c_int)]
+
+
 class sarathi_sched_cfg(ct.Structure):
     _fields_ = [(n, ct.c_int) for n in ("policy", "max_batch", "chunk", "max_chunks", "max_tokens", "n_slots",
                                         "max_seq_len")]
@@ -124,6 +129,8 @@ EXPORTS = {
     "sarathi_linear_scratch_bytes": (ct.c_size_t, [ct.c_int, ct.c_int]),
     "sarathi_linear": (ct.c_int, [ct.c_int, ct.c_int, ct.c_int, ct.c_int, ct.c_int, ct.c_void_p, ct.c_void_p,
                                   ct.c_void_p, ct.c_void_p, ct.c_void_p, ct.c_size_t, ct.c_void_p]),
+    "sarathi_attention_plan": (ct.c_int, [ct.POINTER(sarathi_model_cfg), ct.POINTER(sarathi_hybrid_batch),
+                                          ct.POINTER(sarathi_attn_plan)]),
     "sarathi_linear_plan": (ct.c_int, [ct.c_int, ct.c_int, ct.c_int, ct.c_int, ct.c_int, ct.c_size_t,
                                        ct.POINTER(ct.c_int), ct.POINTER(ct.c_int), ct.POINTER(ct.c_int)]),
     "sarathi_layer_split_scratch_bytes": (ct.c_size_t, [ct.POINTER(sarathi_model_cfg), ct.c_int]),
@@ -331,6 +338,13 @@ def sarathi_linear(dtype, kind, M, N, K, x: int, w: int, resid: int, out: int, s
     rc = lib().sarathi_linear(dtype, kind, M, N, K, ct.c_void_p(x), ct.c_void_p(w), ct.c_void_p(resid or None),
                               ct.c_void_p(out), ct.c_void_p(scratch or None), scratch_bytes, ct.c_void_p(stream))
     return _check(rc) if check else rc
+
+
+def sarathi_attention_plan(cfg: sarathi_model_cfg, batch) -> dict:
+    """Attention work items and key-split partial rows of a layer call."""
+    out = sarathi_attn_plan()
+    _check(lib().sarathi_attention_plan(ct.byref(cfg), ct.byref(batch), ct.byref(out)))
+    return {k: getattr(out, k) for k, _ in sarathi_attn_plan._fields_}
 
 
 def sarathi_linear_plan(dtype, kind, M, N, K, scratch_bytes: int = 0):

@@ -296,3 +296,26 @@ def test_linear_plan_reports_split_choice():
     assert S.sarathi_linear_plan(S.BF16, S.LINEAR_PLAIN, 320, 15360, 5120, scratch)[2] == 1
     with pytest.raises(S.SarathiError):
         S.sarathi_linear_plan(S.BF16, 9, 320, 5120, 5120, 0)
+
+
+def test_attention_plan_counts_partials():
+    from paper_2308_16369_amd import sarathi as S
+    cfg = S.make_cfg(hidden=5120, n_heads=40, head_dim=128, ffn=13824, n_layers=1, dtype=S.BF16)
+    # decodes only: one partial row per 512-key split, every row combined
+    bb, keep = S.make_batch(-1, 0, 0, [1, 2, 3], [10, 600, 1500])
+    p = S.sarathi_attention_plan(cfg, bb)
+    assert p["chunk_items"] == 0 and p["decode_items"] == 1 + 2 + 3
+    assert p["partial_rows_written"] == 6 and p["partial_rows_read"] == 6 and p["combine_rows"] == 3
+    # a short chunk at offset 0 (two key tiles) is one item that writes its rows directly
+    bb, keep = S.make_batch(0, 0, 100, [], [])
+    p = S.sarathi_attention_plan(cfg, bb)
+    assert p == {"chunk_items": 1, "decode_items": 0, "partial_rows_written": 0, "partial_rows_read": 0,
+                 "combine_rows": 0}
+    # a long prefix is split over keys: every split writes the block's rows, the combine reads them all
+    bb, keep = S.make_batch(0, 4096, 100, [7], [5])
+    p = S.sarathi_attention_plan(cfg, bb)
+    assert p["chunk_items"] > 1 and p["decode_items"] == 1
+    assert p["partial_rows_written"] == 100 * p["chunk_items"] + 1
+    assert p["partial_rows_read"] == p["partial_rows_written"] and p["combine_rows"] == 101
+    with pytest.raises(S.SarathiError):
+        S.sarathi_attention_plan(cfg, S.make_batch(-1, 0, 0, [], [])[0])
