@@ -84,6 +84,18 @@ __device__ __forceinline__ int kv_swz(int c, int r) {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
+// Max and sum of the values of lanes l and l ^ 32 (v_permlane32_swap hands
+// each lane both values; no LDS traffic).
+__device__ __forceinline__ f32x2_t lanes_pair(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return f32x2_t{__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
+// Maximum that propagates NaN (v_maximum3_f32; fmaxf would first quieten
+// every matrix-core output).  No score is NaN.
+__device__ __forceinline__ float fmax_nan(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+__device__ __forceinline__ float pair_max(float x) { const f32x2_t p = lanes_pair(x); return fmax_nan(p.x, p.y); }
+__device__ __forceinline__ float pair_sum(float x) { const f32x2_t p = lanes_pair(x); return p.x + p.y; }
+
 // One block = one head x (32 * NW queries of the chunk, one range of keys);
 // wave w owns queries w*32 .. w*32+31.  Per 64-key tile:
 //   S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (A = 32 key rows of the K tile,
@@ -268,9 +280,55 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(PrefillArgs 
   }
   wait_in_flight(NI * (cnt(0, R - 2) + cnt(1, R - 1)));
   lds_read_barrier();
-  if (kbeg <= last_key) scores(kring, s_cur);
+  // ---- mask and running max of one tile's scores.  Keys past the query's
+  // position or the item's end are masked (a tile wholly before every query
+  // of the wave and inside the item needs no mask).  The running max moves
+  // only when a tile's max exceeds it by more than 2^8 (the probabilities of
+  // a tile stay below 256: fp32 sums and bf16 products keep their relative
+  // precision; O and l are rescaled together).
+  auto mask = [&](int kt, floatx16* s) {
+    const int k0 = kbeg + kt * KT;
+    const bool full = k0 + KT <= kend && k0 + KT - 1 <= offset + wq0;
+    if (!full) {
+      const int lim = min(qpos, kend - 1) - k0;   // the lane's last unmasked key, tile-relative
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          if (kb * 32 + 8 * (v >> 2) + 4 * g + (v & 3) > lim) s[kb][v] = -INFINITY;
+    }
+  };
+  auto tile_max = [&](const floatx16* s) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) mx = fmax_nan(mx, s[kb][v]);
+    return pair_max(mx) * scale_log2;   // the query's other keys sit in lane l ^ 32
+  };
+  auto move_max = [&](float mx) {
+    if (__ballot(mx > m_run + 8.0f)) {
+      const float m_new = fmaxf(m_run, mx);
+      // 0 while m_run is -inf; a lane whose keys are all masked so far keeps 1
+      const float corr = (m_new == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f(m_run - m_new);
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) o_acc[db] *= corr;
+      l_run *= corr;
+      m_run = m_new;
+    }
+  };
+  if (kbeg <= last_key) {
+    scores(kring, s_cur);
+    mask(0, s_cur);
+    move_max(tile_max(s_cur));
+  }
 
-  // One tile: scores of tile kt are in sc; the scores of tile kt + 1 go to sn.
+  // One tile: the scores of tile kt are in sc, masked, with the running max
+  // already moved for them; the scores of tile kt + 1 go to sn.  Phase 1:
+  // the matrix cores compute S(kt + 1) while the vector ALU turns S(kt) into
+  // probabilities; phase 2: O += P V of tile kt while the vector ALU masks
+  // S(kt + 1) and takes its max.
+  const f32x2_t ones{1.0f, 1.0f};
   auto step = [&](int kt, floatx16* sc, floatx16* sn) {
     const int k0 = kbeg + kt * KT;
     // K(kt + 1) and V(kt) have landed; after the barrier every wave is done
@@ -282,10 +340,8 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(PrefillArgs 
     // every key of the tile lies past the wave's last query: nothing to add
     // (and none of the later tiles adds anything either)
     if (k0 > last_key) return;
-    // the K fragments of tile kt + 1 are requested first: they arrive while
-    // the vector ALU masks and takes the maximum of tile kt (the K stage of
-    // tile kt + 1 exists in every iteration; past the item's end its stale
-    // values are computed on and never used)
+    // K fragments of tile kt + 1 (its stage exists in every iteration; past
+    // the item's end its stale values are computed on and then masked)
     const uint32_t kn = lds_addr(kring + ((kt + 1) % R) * TILE);
     u32x4 kf[2][D / 16];
 #pragma unroll
@@ -293,77 +349,59 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(PrefillArgs 
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) kf[1][ks] = lds_b128_asm<32 * DCH * 16>(kn + koff[ks]);
 
-    // ---- keys past the query's position or the item's end are masked; a
-    // tile wholly before every query of the wave and inside the item needs
-    // no mask
-    const bool full = k0 + KT <= kend && k0 + KT - 1 <= offset + wq0;
-    if (!full) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int kp = k0 + kb * 32 + 8 * (v >> 2) + 4 * g + (v & 3);
-          if (!(kp <= qpos && kp < kend)) sc[kb][v] = -INFINITY;
-        }
-    }
-    // ---- running max, moved only when a tile's max exceeds it by more than
-    // 2^8 (the probabilities of a tile stay below 256: fp32 sums and bf16
-    // products keep their relative precision; O and l are rescaled together)
-    float mx = -INFINITY;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sc[kb][v]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * scale_log2;
-    if (__ballot(mx > m_run + 8.0f)) {
-      const float m_new = fmaxf(m_run, mx);
-      // 0 while m_run is -inf; a lane whose keys are all masked so far keeps 1
-      const float corr = (m_new == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f(m_run - m_new);
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db) o_acc[db] *= corr;
-      l_run *= corr;
-      m_run = m_new;
-    }
+    // ---- phase 1.  Probabilities p = 2^(s * scale * log2 e - m), rounded to
+    // bf16 (v_cvt_pk_bf16_f32, nearest even); the lane's share of the row
+    // sum adds the rounded pairs (the same values that multiply V).
     const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
-
-    // ---- the scores of tile kt + 1 on the matrix cores, interleaved with the
-    // exponentials of tile kt on the vector ALU
     float sum = 0.f;
     u32x4 pw[4];
-    lds_wait(kf[0]);
-    lds_wait(kf[1]);
+    auto probs = [&](int kb) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-      for (int v = 0; v < 16; ++v) sn[kb][v] = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < D / 16; ++ks)
-        sn[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kf[kb][ks]),
-                                                         __builtin_bit_cast(bf16x8_t, qf[ks]), sn[kb], 0, 0, 0);
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        sc[kb][v] = __builtin_amdgcn_exp2f(fmaf(sc[kb][v], scale_log2, -m_use));
-        sum += sc[kb][v];
-      }
-      // probabilities to bf16 (round to nearest even, v_cvt_pk_bf16_f32)
+      for (int v = 0; v < 16; ++v) sc[kb][v] = __builtin_amdgcn_exp2f(fmaf(sc[kb][v], scale_log2, -m_use));
 #pragma unroll
       for (int h2 = 0; h2 < 2; ++h2) {
         const int vo = h2 * 8;
-        pw[2 * kb + h2] = u32x4{pack_bf16x2(sc[kb][vo], sc[kb][vo + 1]), pack_bf16x2(sc[kb][vo + 2], sc[kb][vo + 3]),
-                                pack_bf16x2(sc[kb][vo + 4], sc[kb][vo + 5]), pack_bf16x2(sc[kb][vo + 6], sc[kb][vo + 7])};
-      }
-      // one matrix product, then about five vector instructions, in turn
+        uint32_t w[4];
 #pragma unroll
-      for (int i = 0; i < D / 16; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+        for (int i = 0; i < 4; ++i) {
+          w[i] = pack_bf16x2(sc[kb][vo + 2 * i], sc[kb][vo + 2 * i + 1]);
+          sum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w[i]),
+                                                __builtin_convertvector(ones, bf16x2_t), sum, false);
+        }
+        pw[2 * kb + h2] = u32x4{w[0], w[1], w[2], w[3]};
       }
+    };
+    probs(0);                                  // while the K fragments arrive
+    asm volatile("" : "+v"(pw[0]), "+v"(pw[1]), "+v"(sum));
+    lds_wait(kf[0]);
+    lds_wait(kf[1]);
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) sn[kb][v] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+        sn[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kf[kb][ks]),
+                                                         __builtin_bit_cast(bf16x8_t, qf[ks]), sn[kb], 0, 0, 0);
+    probs(1);
+    // one matrix product, then three vector instructions, in turn
+#pragma unroll
+    for (int i = 0; i < D / 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
     }
-    sum += __shfl_xor(sum, 32, 64);
+    // the probabilities are complete here (else the compiler would move
+    // their arithmetic next to their use, among the products of phase 2)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) asm volatile("" : "+v"(pw[i]));
+    asm volatile("" : "+v"(sum));
     l_run += sum;
 
-    // ---- O^T += V^T P^T over four 16-key steps; the V fragments of a step
-    // are read while the previous step's products run.
+    // ---- phase 2.  O^T += V^T P^T over four 16-key steps; the V fragments
+    // of a step are read while the previous step's products run.
+    mask(kt + 1, sn);
     const uint32_t vb = lds_addr(vring + (kt % R) * TILE);
     uint32_t va[2][D / 32];
 #pragma unroll
@@ -384,6 +422,7 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(PrefillArgs 
     };
     u32x2 vr[2][2 * (D / 32)];
     vread(vr[0], 0);
+    float mx = -INFINITY;
 #pragma unroll
     for (int ks2 = 0; ks2 < KT / 16; ++ks2) {
       // the next step's V fragments are requested before this step's products
@@ -401,7 +440,11 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(PrefillArgs 
                                                                vc[2 * db + 1].y});
         o_acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, o_acc[db], 0, 0, 0);
       }
+      // a quarter of the next tile's max between the products
+#pragma unroll
+      for (int v = 4 * ks2; v < 4 * ks2 + 4; ++v) mx = fmax_nan(fmax_nan(mx, sn[0][v]), sn[1][v]);
     }
+    move_max(pair_max(mx) * scale_log2);
   };
 
   // two tiles per trip, the score buffers alternating
@@ -409,6 +452,7 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_bf16_kernel(PrefillArgs 
     step(kt, s_cur, s_next);
     if (kt + 1 < n) step(kt + 1, s_next, s_cur);
   }
+  l_run = pair_sum(l_run);               // both halves of the query's keys
 
   // ---- epilogue.  The lane holds column block d of query ql; rows of O (or
   // of the partial) are contiguous in memory, so each wave first transposes
