@@ -316,16 +316,19 @@ static void split_reduce_dispatch(const void* resid, const float* parts, int n_s
                        n_split, n, (To*)out);
 }
 
-// Split-K reduction of rows of N (bf16 residual, fp32 out) followed by the
-// norm of each row, one block per row: the row's sums stay in registers
-// between the reduction and the norm, so the norm reads nothing back.  The
-// sums are formed in split order as in split_reduce_kernel, and the norm
-// accumulates over the same units in the same order as norm_row, so both
-// outputs are bit-identical to the two separate passes.
-template <bool LAYER, int NC>
-__global__ __launch_bounds__(256) void split_reduce_norm_kernel(const bf16* __restrict__ resid,
+// Split-K reduction of rows of N followed by the norm of each row, one block
+// per row: the row's sums stay in registers between the reduction and the
+// norm, so the norm reads nothing back.  RF32 = false: bf16 residual, fp32
+// out (a layer's postproj, then its norm_2); RF32 = true: fp32 residual, bf16
+// out (a layer's ffn_ln2, then the next layer's norm_1, which normalises the
+// bf16-rounded row).  The sums are formed in split order as in
+// split_reduce_kernel, and the norm accumulates over the same units in the
+// same order as norm_row, so both outputs are bit-identical to the two
+// separate passes.
+template <bool LAYER, int NC, bool RF32>
+__global__ __launch_bounds__(256) void split_reduce_norm_kernel(const void* __restrict__ resid_,
                                                                 const float* __restrict__ parts, int n_split, int N,
-                                                                float* __restrict__ out, const bf16* __restrict__ g,
+                                                                void* __restrict__ out_, const bf16* __restrict__ g,
                                                                 const bf16* __restrict__ b, bf16* __restrict__ nout,
                                                                 float eps) {
   __shared__ float red[4];
@@ -352,16 +355,29 @@ __global__ __launch_bounds__(256) void split_reduce_norm_kernel(const bf16* __re
       }
       graw[j] = *reinterpret_cast<const uint4*>(g + (size_t)u * CE);
       if (LAYER) braw[LAYER ? j : 0] = *reinterpret_cast<const uint4*>(b + (size_t)u * CE);
-      Vec16<bf16>::unpack(*reinterpret_cast<const uint4*>(resid + at), v[j]);
+      if constexpr (RF32) {
+        const float4* rp = reinterpret_cast<const float4*>(reinterpret_cast<const float*>(resid_) + at);
+        const float4 lo = rp[0], hi = rp[1];
+        v[j][0] = lo.x; v[j][1] = lo.y; v[j][2] = lo.z; v[j][3] = lo.w;
+        v[j][4] = hi.x; v[j][5] = hi.y; v[j][6] = hi.z; v[j][7] = hi.w;
+      } else {
+        Vec16<bf16>::unpack(*reinterpret_cast<const uint4*>(reinterpret_cast<const bf16*>(resid_) + at), v[j]);
+      }
 #pragma unroll
       for (int sp = 0; sp < MAX_SPLIT; ++sp) {
         if (sp >= n_split) break;
 #pragma unroll
         for (int e = 0; e < CE; ++e) v[j][e] += q[sp][e];
       }
-      float4* op = reinterpret_cast<float4*>(out + at);
-      op[0] = make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
-      op[1] = make_float4(v[j][4], v[j][5], v[j][6], v[j][7]);
+      if constexpr (RF32) {
+        const uint4 w = Store16<bf16>::pack(v[j]);
+        *reinterpret_cast<uint4*>(reinterpret_cast<bf16*>(out_) + at) = w;
+        Vec16<bf16>::unpack(w, v[j]);      // the norm sees the stored (rounded) row
+      } else {
+        float4* op = reinterpret_cast<float4*>(reinterpret_cast<float*>(out_) + at);
+        op[0] = make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
+        op[1] = make_float4(v[j][4], v[j][5], v[j][6], v[j][7]);
+      }
 #pragma unroll
       for (int e = 0; e < CE; ++e) s += v[j][e];
     } else {
@@ -397,13 +413,13 @@ __global__ __launch_bounds__(256) void split_reduce_norm_kernel(const bf16* __re
   }
 }
 
-template <bool LAYER>
+template <bool LAYER, bool RF32>
 static hipError_t split_reduce_norm_layer(const void* resid, const float* parts, int n_split, int rows, int N,
-                                          float* out, const NormArgs& nm, hipStream_t s) {
+                                          void* out, const NormArgs& nm, hipStream_t s) {
   const int nc = (N / 8 + 255) / 256;
-#define SRN_LAUNCH(NCV)                                                                                        \
-  hipLaunchKernelGGL((split_reduce_norm_kernel<LAYER, NCV>), dim3(rows), dim3(256), 0, s, (const bf16*)resid, parts, \
-                     n_split, N, out, (const bf16*)nm.g, (const bf16*)nm.b, (bf16*)nm.out, nm.eps)
+#define SRN_LAUNCH(NCV)                                                                                          \
+  hipLaunchKernelGGL((split_reduce_norm_kernel<LAYER, NCV, RF32>), dim3(rows), dim3(256), 0, s, resid, parts, n_split, \
+                     N, out, (const bf16*)nm.g, (const bf16*)nm.b, (bf16*)nm.out, nm.eps)
   if (nc <= 4) SRN_LAUNCH(4);
   else if (nc <= 8) SRN_LAUNCH(8);
   else SRN_LAUNCH(12);
@@ -411,12 +427,15 @@ static hipError_t split_reduce_norm_layer(const void* resid, const float* parts,
   return hipGetLastError();
 }
 
-hipError_t launch_split_reduce_norm(const void* resid, const float* parts, int n_split, int rows, int N, float* out,
-                                    const NormArgs& norm, hipStream_t s) {
+hipError_t launch_split_reduce_norm(const void* resid, bool resid_f32, const float* parts, int n_split, int rows,
+                                    int N, void* out, const NormArgs& norm, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   if (N % 8 != 0 || N / 8 > 12 * 256 || n_split < 1 || n_split > MAX_SPLIT) return hipErrorNotSupported;
-  return norm.layer ? split_reduce_norm_layer<true>(resid, parts, n_split, rows, N, out, norm, s)
-                    : split_reduce_norm_layer<false>(resid, parts, n_split, rows, N, out, norm, s);
+  if (resid_f32)
+    return norm.layer ? split_reduce_norm_layer<true, true>(resid, parts, n_split, rows, N, out, norm, s)
+                      : split_reduce_norm_layer<false, true>(resid, parts, n_split, rows, N, out, norm, s);
+  return norm.layer ? split_reduce_norm_layer<true, false>(resid, parts, n_split, rows, N, out, norm, s)
+                    : split_reduce_norm_layer<false, false>(resid, parts, n_split, rows, N, out, norm, s);
 }
 
 hipError_t launch_split_reduce(int dtype, bool resid_f32, bool out_f32, const void* resid, const float* parts,

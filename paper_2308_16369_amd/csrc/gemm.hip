@@ -858,8 +858,8 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s, int forc
   }
   if (e != hipSuccess) return e;
   if (n_split > 1) {
-    if (a.norm != nullptr && a.kind == LIN_RESID && dtype == 1) {
-      e = launch_split_reduce_norm(a.resid, a.parts, n_split, a.M, a.N, reinterpret_cast<float*>(a.out), *a.norm, s);
+    if (a.norm != nullptr && resid_kind && dtype == 1) {
+      e = launch_split_reduce_norm(a.resid, a.kind == LIN_RESID_F32IN, a.parts, n_split, a.M, a.N, a.out, *a.norm, s);
       if (e == hipSuccess && a.norm_done) *a.norm_done = true;
       if (e != hipErrorNotSupported) return e;
     }

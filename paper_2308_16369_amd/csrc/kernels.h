@@ -68,10 +68,10 @@ struct LinearArgs {
   // launch_rope_append).
   const RopeArgs* rope;
   bool* rope_done;
-  // LIN_RESID (bf16), optional: the norm of the output rows folded into the
-  // split-K reduction pass when the op runs split over K (then *norm_done =
-  // true and norm->out holds the normalised rows; else the caller runs the
-  // norm).
+  // LIN_RESID / LIN_RESID_F32IN (bf16), optional: the norm of the output
+  // rows folded into the split-K reduction pass when the op runs split over
+  // K (then *norm_done = true and norm->out holds the normalised rows; else
+  // the caller runs the norm).
   const NormArgs* norm;
   bool* norm_done;
 };
@@ -144,10 +144,11 @@ hipError_t launch_attn_combine(int dtype, const CombineArgs& a, hipStream_t s);
 // (resid: fp32 if resid_f32 else dtype; out: fp32 if out_f32 else dtype).
 hipError_t launch_split_reduce(int dtype, bool resid_f32, bool out_f32, const void* resid, const float* parts,
                                int n_split, size_t n, void* out, hipStream_t s);
-// The same for rows x N (bf16 residual, fp32 out) plus the norm of each
-// output row in the same pass (one block per row).  Returns
+// The same for rows x N plus the norm of each output row in the same pass
+// (one block per row): bf16 residual and fp32 out, or (resid_f32) fp32
+// residual and bf16 out, normalised as rounded.  Returns
 // hipErrorNotSupported (nothing launched) when N does not fit one block.
-hipError_t launch_split_reduce_norm(const void* resid, const float* parts, int n_split, int rows, int N, float* out,
-                                    const NormArgs& norm, hipStream_t s);
+hipError_t launch_split_reduce_norm(const void* resid, bool resid_f32, const float* parts, int n_split, int rows,
+                                    int N, void* out, const NormArgs& norm, hipStream_t s);
 
 }  // namespace sarathi

@@ -392,8 +392,14 @@ int upload_meta_rest(const Ctx& c) {
 }
 
 // One decoder layer; metadata already on the device.
+// One layer on the planned batch.  norm1_ready: norm_1 of this layer already
+// sits in the workspace (folded into the previous layer's last reduction);
+// next: the layer after this one in a model step (null for the last layer or
+// a single-layer call), whose norm_1 is folded into this layer's ffn_ln2
+// split-K reduction when that op runs split (*next_norm1_done says so).
 int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const void* x_in, void* x_out,
-               bool carry_meta) {
+               bool carry_meta, bool norm1_ready = false, const sarathi_layer_weights* next = nullptr,
+               bool* next_norm1_done = nullptr) {
   const sarathi_model_cfg* cfg = c.cfg;
   const Plan& P = *c.plan;
   const int T = P.T, H = cfg->hidden, nh = cfg->n_heads, hd = cfg->head_dim, F = cfg->ffn;
@@ -418,7 +424,9 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
 
   // norm_1
   SARATHI_MARK();
-  if (carry_meta) {
+  if (norm1_ready) {
+    e = hipSuccess;
+  } else if (carry_meta) {
     MetaChunk first;
     meta_chunk(P, 0, &first);
     e = launch_norm(dt, false, ln, x_in, w->norm1_g, w->norm1_b, ws + c.L.a, T, H, cfg->eps, c.s, &first,
@@ -510,6 +518,11 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
   LinearArgs dn{};
   dn.kind = LIN_RESID_F32IN; dn.M = T; dn.N = H; dn.K = F; dn.x = ws + c.L.m; dn.w = w->w_down; dn.resid = hres;
   dn.out = x_out; dn.parts = parts; dn.parts_cap = parts_cap;
+  NormArgs n1{};
+  if (next != nullptr && next_norm1_done != nullptr) {
+    n1 = NormArgs{next->norm1_g, next->norm1_b, ws + c.L.a, cfg->eps, ln};
+    dn.norm = &n1; dn.norm_done = next_norm1_done;   // 'a' is free: ffn_ln1 has read it
+  }
   e = launch_linear(dt, dn, c.s);
   if (e != hipSuccess) return hip_fail(e, "ffn_ln2");
   SARATHI_MARK();
@@ -673,11 +686,14 @@ int run_model(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, sara
   if (rc) return rc;
   char* ping[2] = {c.ws + L.ping0, c.ws + L.ping1};
   const int n = cfg->n_layers;
+  bool norm1_ready = false;
   for (int l = 0; l < n; ++l) {
     const void* in = (l == 0) ? x_in : ping[l & 1];
     void* out = (l == n - 1) ? x_out : ping[(l + 1) & 1];
-    rc = layer_body(c, w + l, l, in, out, l == 0);
+    bool next_ready = false;
+    rc = layer_body(c, w + l, l, in, out, l == 0, norm1_ready, l + 1 < n ? w + l + 1 : nullptr, &next_ready);
     if (rc) return rc;
+    norm1_ready = next_ready;
   }
   return SARATHI_OK;
 }
