@@ -351,18 +351,21 @@ __global__ __launch_bounds__(64 * (WGM * WGN + NP)) void gemm_ws_kernel(GemmP p)
 
   if (wave >= NC) {
     // ---------------- producer
-    const int q = wave - NC;
-    const bf16* A = reinterpret_cast<const bf16*>(p.A);
-    const bf16* W = reinterpret_cast<const bf16*>(p.W);
+    // The wave index is uniform: the LDS destinations (m0) and the matrix
+    // bases are scalar, and each lane keeps one 32-bit byte offset per row
+    // group, so a request costs no vector instruction (global_load_lds with
+    // a scalar base; the launcher keeps both matrices below 4 GiB).
+    const int q = __builtin_amdgcn_readfirstlane(wave - NC);
+    const char* A = reinterpret_cast<const char*>(p.A) + (size_t)kbeg * 2;
+    const char* W = reinterpret_cast<const char*>(p.W) + (size_t)kbeg * 2;
     const int lchunk = (lane & 7) ^ (lane >> 3);
-    const bf16* src[IHI];
+    uint32_t off[IHI];
 #pragma unroll
     for (int j = 0; j < IHI; ++j) {
       const int g = min(j * NP + q, G - 1);
       const int row = g * 8 + (lane >> 3);
-      const size_t r = g < GA ? (size_t)min(m0 + row, p.M - 1) : 0;
-      src[j] = g < GA ? A + r * p.K + kbeg + lchunk * 8
-                      : W + (size_t)w_row_of<EPI, WTN>(row - BM, n0_out, p.N) * p.K + kbeg + lchunk * 8;
+      const size_t r = g < GA ? (size_t)min(m0 + row, p.M - 1) : (size_t)w_row_of<EPI, WTN>(row - BM, n0_out, p.N);
+      off[j] = (uint32_t)(r * p.K * 2 + lchunk * 16);
     }
     const bool extra = q < RHI;
     // With rotate_k, the G = tiles_m blocks that share a W panel take each
@@ -377,9 +380,11 @@ __global__ __launch_bounds__(64 * (WGM * WGN + NP)) void gemm_ws_kernel(GemmP p)
         if (base + GR <= nk) kt = base + (kt - base + tile_m * RD) % GR;
       }
       uint4* dst = lds + stage * ROWS * 8;
+      const char* a_k = A + (size_t)kt * BK * 2;
+      const char* w_k = W + (size_t)kt * BK * 2;
 #pragma unroll
       for (int j = IHI - 1; j >= 0; --j)
-        if (j < ILO || extra) dma16(src[j] + (size_t)kt * BK, dst + (j * NP + q) * 64);
+        if (j < ILO || extra) dma16((min(j * NP + q, ROWS / 8 - 1) < GA ? a_k : w_k) + off[j], dst + (j * NP + q) * 64);
     };
     auto wait_next = [&](bool all) {   // all but the newest S - 2 stages landed
       if (all) wait_vmcnt<0>();
@@ -776,7 +781,10 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s, int forc
   }
   const bool swiglu = a.kind == LIN_SWIGLU;
   const bool resid_kind = a.kind == LIN_RESID || a.kind == LIN_RESID_F32IN;
-  const bool ws = (a.K % 64) == 0;   // producer/consumer kernel: whole 64-wide k-tiles
+  // producer/consumer kernel: whole 64-wide k-tiles, and x and W each under
+  // 4 GiB (its producers address rows by 32-bit byte offsets)
+  const size_t w_rows = swiglu ? 2 * (size_t)a.N : (size_t)a.N;
+  const bool ws = (a.K % 64) == 0 && (size_t)a.M * a.K * 2 < (1ull << 32) && w_rows * a.K * 2 < (1ull << 32);
 
   // splits available to the residual ops: whole groups of two k-tiles per
   // split, partials must fit the scratch
