@@ -19,7 +19,12 @@ through the C-ABI:
   whole 40-layer LLaMA-13B model: a prefill-only iteration of 1024 tokens, a
   decode-only iteration of 4 decodes at sequence length 1024, and a
   decode-maximal iteration of one 1021-token chunk plus 3 decodes, each split
-  into linear-op, attention and other time.
+  into linear-op, attention and other time;
+* a tile sweep of the four linear ops of a workload's layer: every
+  producer/consumer tile shape (and, for the residual ops, the split-K count
+  the planner would use) timed alone through sarathi_linear_tiled, next to
+  the planner's pick; preproj tiles that hold whole heads (the ones whose
+  epilogue can take the rotary embedding and the KV append) are marked.
 
 Inputs are seeded synthetic tensors drawn on the device (weights
 0.02 * N(0,1), activations and cached K/V N(0,1)); only timing is measured
@@ -362,6 +367,75 @@ def to_markdown(res: dict) -> str:
     return out
 
 
+def tile_sweep(shape, T: int, iters: int = 20) -> List[dict]:
+    """Every producer/consumer tile of the four linear ops over T rows, each op
+    alone (split reductions included), with the planner's pick."""
+    import torch
+
+    from . import sarathi as S
+
+    def _time(fn: Callable[[], None], n: int) -> float:   # ms per call, events on the null stream fn uses
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    H, nh, d, F = shape.hidden, shape.n_heads, shape.head_dim, shape.ffn
+    QD = nh * d
+    dt = torch.bfloat16
+    up_kind = S.LINEAR_SWIGLU if shape.act == "swiglu" else S.LINEAR_GELU
+    ops = [("preproj", S.LINEAR_PLAIN, 3 * QD, H, 3 * QD), ("postproj", S.LINEAR_RESID, H, QD, H),
+           ("ffn_ln1", up_kind, F, H, shape.up_rows), ("ffn_ln2", S.LINEAR_RESID_F32IN, H, F, H)]
+    scratch_bytes = S.sarathi_linear_scratch_bytes(T, max(H, F))
+    scratch = torch.empty(scratch_bytes // 4 + 1, dtype=torch.float32, device="cuda")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(7)
+    out: List[dict] = []
+    for name, kind, N, K, w_rows in ops:
+        x = (torch.randn(T, K, generator=g, device="cuda") * 0.5).to(dt)
+        w = (torch.randn(w_rows, K, generator=g, device="cuda") * 0.02).to(dt)
+        resid_dt = torch.float32 if kind == S.LINEAR_RESID_F32IN else dt
+        out_dt = torch.float32 if kind == S.LINEAR_RESID else dt
+        resid = torch.randn(T, N, generator=g, device="cuda").to(resid_dt)
+        y = torch.empty(T, N, dtype=out_dt, device="cuda")
+        pick = S.sarathi_linear_plan(S.BF16, kind, T, N, K, scratch_bytes)
+        splits = sorted({1, pick[2]}) if kind in (S.LINEAR_RESID, S.LINEAR_RESID_F32IN) else [1]
+        for tile in range(S.sarathi_linear_tile_count()):
+            bm, bn = S.sarathi_linear_tile_shape(tile)
+            if bm == 64 and T > 64:
+                continue
+            for ns in splits:
+                run = lambda: S.sarathi_linear_tiled(kind, T, N, K, x.data_ptr(), w.data_ptr(), resid.data_ptr(),
+                                                     y.data_ptr(), scratch.data_ptr(), scratch_bytes, tile, ns)
+                for _ in range(3):
+                    run()
+                ms = _time(run, iters)
+                out.append({"op": name, "T": T, "N": N, "K": K, "bm": bm, "bn": bn, "n_split": ns, "us": ms * 1e3,
+                            "tflops": 2.0 * T * w_rows * K / (ms * 1e-3) / 1e12,
+                            "picked": (bm, bn, ns) == tuple(pick),
+                            "whole_heads": name == "preproj" and bn % d == 0 and QD % bn == 0})
+        del x, w, resid, y
+    return out
+
+
+def tile_sweep_markdown(workload: str, rows: List[dict]) -> str:
+    lines = [f"## Linear-op tile sweep: {workload} (T = {rows[0]['T']} rows)\n",
+             "Each op alone through `sarathi_linear_tiled` (split-K reductions included), mean of 20 calls after "
+             "3 warm-ups; weights re-read every call (a 256 MB memory-side cache can hold one "
+             "op's weights between calls, so these times can be below the in-layer ones).  * = the planner's "
+             "pick; h = a preproj tile that holds whole heads (its epilogue can take RoPE + KV append).\n",
+             "| op | N x K | tile (BM x BN) | K-splits | us | TFLOP/s | |", "|---|---|---|---|---|---|---|"]
+    for e in rows:
+        mark = ("*" if e["picked"] else "") + ("h" if e["whole_heads"] else "")
+        lines.append(f"| {e['op']} | {e['N']} x {e['K']} | {e['bm']} x {e['bn']} | {e['n_split']} | {e['us']:.1f} | "
+                     f"{e['tflops']:.0f} | {mark} |")
+    return "\n".join(lines) + "\n"
+
+
 def main(argv: Optional[Sequence[str]] = None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--workload", default="llama13b", choices=["llama13b", "tiny"])
@@ -370,6 +444,8 @@ def main(argv: Optional[Sequence[str]] = None) -> int:
     ap.add_argument("--quick", action="store_true", help="a few points of each sweep")
     ap.add_argument("--table2-only", action="store_true", help="only the whole-model per-token table")
     ap.add_argument("--no-table2", action="store_true", help="skip the whole-model per-token table")
+    ap.add_argument("--tile-sweep", nargs="+", default=None, metavar="WORKLOAD",
+                    help="only the linear-op tile sweep of these workloads (names in workloads.WORKLOADS)")
     args = ap.parse_args(argv)
 
     import torch
@@ -377,6 +453,24 @@ def main(argv: Optional[Sequence[str]] = None) -> int:
     import workloads as wl
 
     assert torch.cuda.is_available(), "the ablation runs on a GPU"
+    if args.tile_sweep:
+        cmd = "python -m paper_2308_16369_amd.ablation " + " ".join(argv if argv is not None else sys.argv[1:])
+        res = {"command": cmd, "tile_sweep": {}}
+        md = [f"# Linear-op tile sweeps\n\nCommand: `{cmd}`\n"]
+        for name in args.tile_sweep:
+            w = wl.WORKLOADS[name]
+            T = w.batch.chunk_len + w.batch.n_decodes
+            rows = tile_sweep(w.shape, T)
+            res["tile_sweep"][name] = rows
+            md.append(tile_sweep_markdown(name, rows))
+            print(f"# {name}: {len(rows)} points", file=sys.stderr, flush=True)
+        if args.json:
+            with open(args.json, "w") as f:
+                json.dump(res, f, indent=1)
+        if args.md:
+            with open(args.md, "w") as f:
+                f.write("\n".join(md))
+        return 0
     if args.workload == "llama13b":
         shape = wl.LLAMA13B_LAYER.shape
         prompts = [1024, 2048] if args.quick else [1024, 2048, 3072]
