@@ -131,6 +131,28 @@ def per_call_ms(make_call, stream, steps):
     return [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
 
 
+def cold_call_ms(make_call, stream, steps, flush_bytes=1 << 30):
+    """Time of each of ``steps`` calls made with cold caches: before each
+    call a 1 GiB buffer is read on the same stream (more than the 256 MB
+    memory-side cache and the L2s hold; a read leaves clean lines behind,
+    so no write-back lands inside the call), then HIP events bracket the
+    call alone."""
+    import torch
+    call, keep = make_call()
+    buf = torch.ones(flush_bytes // 4, dtype=torch.float32, device="cuda")
+    call()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    torch.cuda.synchronize()
+    for i in range(steps):
+        buf.sum()
+        ev[i][0].record(stream)
+        call()
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    del buf
+    return [a.elapsed_time(b) for a, b in ev]
+
+
 def oracle_cpu_baseline(oracle, shp, w, kv_layer, ob, x, T, budget_s=25.0, one_core_max_s=45.0):
     """The oracle on the host cores: one full layer call of the workload,
     one untimed warm-up, then the median of up to 3 calls within budget_s
@@ -384,6 +406,8 @@ def main():
     print(f"# hybrid: {ms:.4f} ms/step with stage events, {ms_plain:.4f} without", file=sys.stderr, flush=True)
     # ---- spread: the same steps with one event between consecutive calls
     per_call = per_call_ms(lambda: run_once(b, x, y), stream, args.steps)
+    # ---- cold caches: each call after a 1 GiB write (outside the timed region above)
+    cold = cold_call_ms(lambda: run_once(b, x, y), stream, max(args.steps, 10))
 
     # ---- decode accounting (Sec. 5.1.1): prefill-only and decode-only batches of the same rows
     extra = {}
@@ -496,6 +520,10 @@ def main():
         "layer_roofline": {"ms": round(roof_ms, 5), "frac": round(roof_ms / ms_plain, 4),
                            "overhead_bytes": round(over_total)},
         "ms_per_call_p10_p50_p90": [round(float(np.percentile(per_call, q)), 5) for q in (10, 50, 90)],
+        "cold": {"ms_per_call_p10_p50_p90": [round(float(np.percentile(cold, q)), 5) for q in (10, 50, 90)],
+                 "tokens_per_s_p50": round(T / (float(np.median(cold)) * 1e-3), 1),
+                 "calls": len(cold), "note": "each call timed alone after a 1 GiB read that evicts the "
+                                             "memory-side cache and the L2s"},
         "ms_per_step_with_stage_events": round(ms, 5),
         "wall_ms_per_step": round(wall_ms, 5),
         "linear_ops": {"ms": round(lin_ms, 5), "mfma_frac": round(lin_mfma, 4),
