@@ -404,6 +404,18 @@ def tile_sweep(shape, T: int, iters: int = 20) -> List[dict]:
         y = torch.empty(T, N, dtype=out_dt, device="cuda")
         pick = S.sarathi_linear_plan(S.BF16, kind, T, N, K, scratch_bytes)
         splits = sorted({1, pick[2]}) if kind in (S.LINEAR_RESID, S.LINEAR_RESID_F32IN) else [1]
+        if K % 64 != 0:
+            # no tile choice for a K off the 64-wide k-tiles: the op's one kernel, as the planner runs it
+            run = lambda: S.sarathi_linear(S.BF16, kind, T, N, K, x.data_ptr(), w.data_ptr(), resid.data_ptr(),
+                                           y.data_ptr(), scratch.data_ptr(), scratch_bytes)
+            for _ in range(3):
+                run()
+            ms = _time(run, iters)
+            out.append({"op": name, "T": T, "N": N, "K": K, "bm": pick[0], "bn": pick[1], "n_split": pick[2],
+                        "us": ms * 1e3, "tflops": 2.0 * T * w_rows * K / (ms * 1e-3) / 1e12, "picked": True,
+                        "whole_heads": False})
+            del x, w, resid, y
+            continue
         for tile in range(S.sarathi_linear_tile_count()):
             bm, bn = S.sarathi_linear_tile_shape(tile)
             if bm == 64 and T > 64:
