@@ -102,17 +102,19 @@ __device__ __forceinline__ float pair_sum(float x) { const f32x2_t p = lanes_pai
 //     B = the wave's Q^T fragments held in registers), two 32-key blocks;
 //     lane l holds, per block, the 16 scores of query l % 32 for keys
 //     8*(v/4) + 4*(l/32) + v%4;
-//   the online softmax runs on each query's registers (+1 lane exchange
-//     with lane l ^ 32, which holds the query's other keys);
+//   the online softmax runs on each query's registers (the query's other
+//     keys sit in lane l ^ 32: one lane swap for the max, one for the sum
+//     at the end);
 //   O^T += V^T P^T (32x32x16: B = the lane's probabilities packed as bf16x8
 //     straight from registers, A = V^T fragments from transposed LDS reads).
 //     The product's k order is a permutation of each 16-key step: lane
 //     group g = l / 32 supplies keys 4g..4g+3 and 8+4g..8+4g+3, which is what
 //     two transposed reads of those four rows deliver.
 // Each LDS byte of K and V feeds 32 queries (twice the 16 of a 16x16 tile).
-// Software pipeline: while the vector ALU runs the softmax of tile k, the
-// matrix cores already compute the scores of tile k + 1 (issued first, no
-// dependency between the two), then O += P V of tile k.  K and V tiles sit
+// Software pipeline, per tile k: the matrix cores compute the scores of
+// tile k + 1 while the vector ALU turns the scores of tile k into
+// probabilities; then O += P V of tile k while the vector ALU masks the
+// scores of tile k + 1 and takes their max.  K and V tiles sit
 // in two R-stage LDS rings; iteration k reads K(k + 1) and V(k) and
 // requests V(k + R - 1) and K(k + R) into the stages of V(k - 1) and K(k),
 // so R - 2 tiles of each are in flight while one is used (R = 4: 128 KB
@@ -120,10 +122,10 @@ __device__ __forceinline__ float pair_sum(float x) { const f32x2_t p = lanes_pai
 // latency of tiles that come from HBM).  Tiles arrive by LDS DMA
 // (global_load_lds_dwordx4: a wave instruction fills 1 KB = 1024 / (2 D) key
 // rows; lane i takes LDS slot i of its row and so reads the chunk that the
-// swizzle puts there); one barrier per tile.  A wave skips the arithmetic of tiles wholly past its last query
-// (the causal triangle of the chunk).
+// swizzle puts there); one barrier per tile.  A wave skips the arithmetic
+// of tiles wholly past its last query (the causal triangle of the chunk).
 // Output: a work item with partial index p >= 0 writes the partial
-// [m, l, o[D]] of each of its rows (merged by the combine pass); p < 0 means
+// [m, l, -, -, o[D]] of each of its rows (merged by the combine pass); p < 0 means
 // the item covers all of its rows' keys, and it writes the normalised rows
 // of O (dtype bf16) directly.
 template <int D, int NW, int R>
