@@ -7,8 +7,9 @@
 // Chunked-prefill attention (bf16, MFMA): the chunk's queries at positions
 // off..off+C-1 attend to the prefill slot's keys 0..position (the earlier
 // chunks' cached keys plus, causally, the chunk's own; Sec. 4.2).  Work item
-// = (block of PREFILL_QBLOCK queries, a range of 64-key tiles), one head per
-// block of PREFILL_QBLOCK / 32 waves x 32 query rows.  K and V tiles of 64
+// = (block of qblock queries, a range of 64-key tiles), one head per block of
+// qblock / 32 waves x 32 query rows; qblock is PREFILL_QBLOCK (8 waves) or
+// PREFILL_QBLOCK_SMALL (4 waves), chosen per batch by the plan.  K and V tiles of 64
 // keys are staged in LDS rings by LDS DMA (V read back transposed so P*V
 // takes 16 contiguous bytes per lane); S = Q K^T and O += P V run on
 // v_mfma_f32_32x32x16_bf16 with an fp32 online softmax.
@@ -529,10 +530,15 @@ hipError_t launch_attn_prefill(int dtype, const PrefillArgs& a, hipStream_t s) {
   if (dtype != 1) return hipErrorInvalidValue;
   const float scale_log2 = LOG2E / sqrtf((float)a.hd);
   const unsigned grid = (unsigned)(((size_t)a.n_work * a.nh + 7) / 8 * 8);
-  constexpr int NW = PREFILL_QBLOCK / 32;
-  // 4-deep K and V rings: 128 KB for head_dim 128, one block of 8 waves per CU
-  if (a.hd == 128) return run_prefill<128, NW, 4>(a, grid, scale_log2, s);
-  return run_prefill<64, NW, 4>(a, grid, scale_log2, s);
+  // 256-row q-blocks: 8 waves, 4-deep K and V rings (128 KB for head_dim 128,
+  // one block per CU); 128-row q-blocks: 4 waves, 3-deep rings (96 KB)
+  if (a.qblock == PREFILL_QBLOCK_SMALL) {
+    if (a.hd == 128) return run_prefill<128, PREFILL_QBLOCK_SMALL / 32, 3>(a, grid, scale_log2, s);
+    return run_prefill<64, PREFILL_QBLOCK_SMALL / 32, 3>(a, grid, scale_log2, s);
+  }
+  if (a.qblock != PREFILL_QBLOCK) return hipErrorInvalidValue;
+  if (a.hd == 128) return run_prefill<128, PREFILL_QBLOCK / 32, 4>(a, grid, scale_log2, s);
+  return run_prefill<64, PREFILL_QBLOCK / 32, 4>(a, grid, scale_log2, s);
 }
 
 }  // namespace sarathi

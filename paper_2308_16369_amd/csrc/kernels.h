@@ -96,7 +96,12 @@ bool linear_tile_shape(int tile, int* bm, int* bn);
 // of the log2-scaled scores, l the sum of 2^(s - m), o the unnormalised
 // weighted sum of values.
 constexpr int PART_O = 4;
-constexpr int PREFILL_QBLOCK = 256;   // chunk rows per chunk-attention work item (8 waves x 32)
+// Chunk rows per chunk-attention work item: 256 (8 waves x 32 queries, two
+// waves per SIMD) for long chunks and long prefixes, 128 (4 waves x 32, one
+// per SIMD, a smaller block set-up and output) for short ones; the host's plan
+// picks one per batch.  Buffers are sized for the larger.
+constexpr int PREFILL_QBLOCK = 256;
+constexpr int PREFILL_QBLOCK_SMALL = 128;
 struct PrefillArgs {
   const void* qkv;      // all rows; chunk c's rows start at its first-row entry; q columns rotated
   int ld_qkv;
@@ -106,7 +111,8 @@ struct PrefillArgs {
   int nh, hd;
   const int* work;      // [n_work][chunk, q_block, partial slot p, (first key tile << 16) | end key tile]
   int n_work;
-  float* part;          // row j of an item's q-block -> partial index p * PREFILL_QBLOCK + j
+  int qblock;           // rows per q-block: PREFILL_QBLOCK or PREFILL_QBLOCK_SMALL
+  float* part;          // row j of an item's q-block -> partial index p * qblock + j
   void* out;            // p < 0 (the item covers every key of its rows): normalised rows of O [T, nh*hd]
   int ld_out;
 };

@@ -51,7 +51,7 @@ int hip_fail(hipError_t e, const char* what) {
 
 constexpr int SPLIT_KEYS = 512;   // keys per decode-attention work item
 constexpr int PRE_SPLIT = 256;    // smallest key split of a chunk-attention work item
-constexpr int QBLOCK = PREFILL_QBLOCK;   // chunk rows per chunk-attention work item
+constexpr int QBLOCK = PREFILL_QBLOCK;   // chunk rows per chunk-attention work item (the larger size)
 constexpr int PARTS_ROWS = 512;   // split-K partials are sized for batches up to this many rows (larger
                                   // batches fill the GPU without splitting; with less room fewer splits run)
 
@@ -166,6 +166,7 @@ int from_mixed(const sarathi_mixed_batch* b, BatchDesc* out) {
 // Host-side description of the batch and its device metadata.
 struct Plan {
   int C, B, T, row_base, n_pre, n_dec, n_chunks, pre_tiles;
+  int qblock;      // chunk rows per chunk-attention q-block (PREFILL_QBLOCK or PREFILL_QBLOCK_SMALL)
   int pre_slots;   // partial q-block slots of the chunk items (items covering all keys of their rows write O)
   int comb_row0;   // first row whose attention output the combine pass writes
   // row_slot[T] row_pos[T] comb[3T] chunk table [n_chunks][slot, offset, len, first row]
@@ -213,11 +214,12 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
   p.T = p.C + p.B;
   p.n_chunks = (int)b.chunks.size();
   // bf16: chunk rows go to the MFMA chunk-attention kernel (work item = one
-  // chunk's 64-row query block x key split), decodes to row attention (work
+  // chunk's query block x key split), decodes to row attention (work
   // item = row x key split).  fp32: every row goes to row attention (a chunk
   // row at position p is attention over keys 0..p, like a decode with ctx = p).
   p.row_base = (cfg->dtype == SARATHI_BF16) ? p.C : 0;
   p.pre_tiles = PRE_SPLIT / 64;
+  p.qblock = QBLOCK;
   p.pre_slots = 0;
   std::vector<int> slot(p.T), pos(p.T), comb(3 * p.T), tab, pre, dec;
   int r0 = 0;
@@ -229,7 +231,7 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
   for (int i = 0; i < p.B; ++i) { slot[p.C + i] = b.dslots[i]; pos[p.C + i] = b.dctx[i]; }
   if (p.row_base > 0) {
     // Partial slots run q-block by q-block (a row's splits are consecutive,
-    // QBLOCK partial rows apart); the work items run split by split so that
+    // qblock partial rows apart); the work items run split by split so that
     // the query blocks that read the same keys are neighbours (and share an
     // XCD's L2, see the chunk-attention kernel).
     // Key ranges: each q-block's keys, in 64-key tiles, are cut into ns
@@ -237,30 +239,42 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
     // minimises rounds of blocks (one per CU) x (largest range + ~4 tiles of
     // fixed cost per block), fitted to measurements of the LLaMA-33B and
     // GPT-3 chunk shapes; ties go to the larger tau (fewer partials).
+    // Two q-block sizes are priced the same way: a 128-row block (4 waves,
+    // one per SIMD) takes ~0.82x the time of a 256-row block per key tile
+    // (measured on the LLaMA-13B, LLaMA-33B and GPT-3 chunk shapes), and
+    // wins when the chunk is short or the heads few (fewer idle waves and a
+    // smaller set-up and output per block).
     std::vector<int> qtiles;   // tiles of every q-block, chunk by chunk
-    int t_max = 1;
-    for (const ChunkDesc& c : b.chunks)
-      for (int qb = 0; qb * QBLOCK < c.len; ++qb) {
-        const int n_keys = c.offset + std::min((qb + 1) * QBLOCK, c.len);
-        qtiles.push_back((n_keys + 63) / 64);
-        t_max = std::max(t_max, qtiles.back());
-      }
-    const int tau_min = PRE_SPLIT / 64;
-    int tau = tau_min;
+    int tau = PRE_SPLIT / 64;
     double best = 1e300;
-    for (int cand = tau_min; cand <= std::max(t_max, tau_min); cand += std::max(1, cand / 4)) {
-      long blocks = 0;
-      int longest = 0;
-      for (int t : qtiles) {
-        const int ns = (t + cand - 1) / cand;
-        blocks += ns;
-        longest = std::max(longest, (t + ns - 1) / ns);
-      }
-      blocks *= cfg->n_heads;
-      const double cost = (double)((blocks + 255) / 256) * (longest + 4);
-      if (cost <= best) {
-        best = cost;
-        tau = cand;
+    p.qblock = QBLOCK;
+    for (const int qbs : {QBLOCK, PREFILL_QBLOCK_SMALL}) {
+      const double per_tile = qbs == QBLOCK ? 1.0 : 0.82;
+      std::vector<int> qt;
+      int t_max = 1;
+      for (const ChunkDesc& c : b.chunks)
+        for (int qb = 0; qb * qbs < c.len; ++qb) {
+          const int n_keys = c.offset + std::min((qb + 1) * qbs, c.len);
+          qt.push_back((n_keys + 63) / 64);
+          t_max = std::max(t_max, qt.back());
+        }
+      const int tau_min = PRE_SPLIT / 64;
+      for (int cand = tau_min; cand <= std::max(t_max, tau_min); cand += std::max(1, cand / 4)) {
+        long blocks = 0;
+        int longest = 0;
+        for (int t : qt) {
+          const int ns = (t + cand - 1) / cand;
+          blocks += ns;
+          longest = std::max(longest, (t + ns - 1) / ns);
+        }
+        blocks *= cfg->n_heads;
+        const double cost = (double)((blocks + 255) / 256) * (longest + 4) * per_tile;
+        if (cost <= best) {
+          best = cost;
+          tau = cand;
+          p.qblock = qbs;
+          qtiles = qt;
+        }
       }
     }
     p.pre_tiles = tau;
@@ -271,7 +285,7 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
     // consecutive partial slots
     for (int ci = 0; ci < p.n_chunks; ++ci) {
       const ChunkDesc& c = b.chunks[ci];
-      const int nqb = (c.len + QBLOCK - 1) / QBLOCK;
+      const int qbs = p.qblock, nqb = (c.len + qbs - 1) / qbs;
       std::vector<int> ns(nqb), first(nqb), nt(nqb);
       int max_ns = 0;
       for (int qb = 0; qb < nqb; ++qb) {
@@ -280,10 +294,10 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
         first[qb] = ns[qb] > 1 ? slot_base : -1;
         if (ns[qb] > 1) slot_base += ns[qb];
         max_ns = std::max(max_ns, ns[qb]);
-        for (int r = qb * QBLOCK; r < std::min((qb + 1) * QBLOCK, c.len); ++r) {
-          comb[3 * (r0 + r)] = ns[qb] > 1 ? first[qb] * QBLOCK + (r - qb * QBLOCK) : 0;
+        for (int r = qb * qbs; r < std::min((qb + 1) * qbs, c.len); ++r) {
+          comb[3 * (r0 + r)] = ns[qb] > 1 ? first[qb] * qbs + (r - qb * qbs) : 0;
           comb[3 * (r0 + r) + 1] = ns[qb] > 1 ? ns[qb] : 0;
-          comb[3 * (r0 + r) + 2] = QBLOCK;
+          comb[3 * (r0 + r) + 2] = qbs;
         }
       }
       for (int s = 0; s < max_ns; ++s)
@@ -296,7 +310,7 @@ Plan make_plan(const sarathi_model_cfg* cfg, const BatchDesc& b) {
     }
     p.pre_slots = slot_base;
   }
-  const int pre_rows = p.pre_slots * QBLOCK;
+  const int pre_rows = p.pre_slots * p.qblock;
   // Row-attention items run in the order of the rows' KV slots (each row's
   // splits together), so the blocks in flight stream the cache in address
   // order (measured ~2% faster than a random slot order).
@@ -463,7 +477,7 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
     PrefillArgs pa{};
     pa.qkv = ws + c.L.qkv; pa.ld_qkv = 3 * QD; pa.kv_layer = kv_layer; pa.st = c.kv->st;
     pa.chunks = meta + P.o_chunks; pa.nh = nh; pa.hd = hd;
-    pa.work = meta + P.o_pre; pa.n_work = P.n_pre; pa.part = part;
+    pa.work = meta + P.o_pre; pa.n_work = P.n_pre; pa.qblock = P.qblock; pa.part = part;
     pa.out = ws + c.L.o; pa.ld_out = QD;
     e = launch_attn_prefill(dt, pa, c.s);
     if (e != hipSuccess) return hip_fail(e, "chunk attention");
@@ -474,7 +488,7 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
     da.qkv = ws + c.L.qkv; da.ld_qkv = 3 * QD; da.kv_layer = kv_layer; da.st = c.kv->st;
     da.row_slot = meta + P.o_slot; da.row_pos = meta + P.o_pos; da.work = meta + P.o_dec;
     da.row_base = P.row_base; da.n_work = P.n_dec; da.split_keys = SPLIT_KEYS; da.nh = nh; da.hd = hd;
-    da.part = part; da.part_base = P.pre_slots * QBLOCK;
+    da.part = part; da.part_base = P.pre_slots * P.qblock;
     e = launch_attn_rows(dt, da, c.s);
     if (e != hipSuccess) return hip_fail(e, "decode attention");
   }
@@ -571,7 +585,7 @@ int prepare(const sarathi_model_cfg* cfg, const sarathi_layer_weights* w, int n_
   // the plan must fit the regions the layout sized for it (an internal
   // invariant: the bounds above hold for every batch check_batch accepts)
   const size_t part_rows = (L->meta - L->part) / ((size_t)cfg->n_heads * (cfg->head_dim + PART_O) * 4);
-  if (plan->meta.size() * 4 > L->ping0 - L->meta || (size_t)plan->pre_slots * QBLOCK + plan->n_dec > part_rows)
+  if (plan->meta.size() * 4 > L->ping0 - L->meta || (size_t)plan->pre_slots * plan->qblock + plan->n_dec > part_rows)
     return fail(SARATHI_EINVAL, "internal: batch plan exceeds its workspace layout");
   return SARATHI_OK;
 }
@@ -838,8 +852,8 @@ int sarathi_attention_plan(const sarathi_model_cfg* cfg, const sarathi_hybrid_ba
   long written = P.n_dec;
   for (int i = 0; i < P.n_pre; ++i)
     if (pre[4 * i + 2] >= 0) {
-      const int len = chunks[4 * pre[4 * i] + 2], q0 = pre[4 * i + 1] * QBLOCK;
-      written += std::min(QBLOCK, len - q0);
+      const int len = chunks[4 * pre[4 * i] + 2], q0 = pre[4 * i + 1] * P.qblock;
+      written += std::min(P.qblock, len - q0);
     }
   o.partial_rows_written = written;
   for (int r = 0; r < P.T; ++r)
