@@ -246,14 +246,26 @@ __device__ __forceinline__ int w_row_of(int nl, int n0_out, int N) {
   return min(n0_out + nl, N - 1);
 }
 
-// Epilogue of preproj with the rotary embedding and the KV append fused (the
-// "others" of Sec. 2.1 that follow the QKV matmul): the block's tile (whole
-// heads of q, k or v: BN a multiple of head_dim, the [q|k|v] parts a multiple
-// of BN) goes to LDS as bf16 -- the rounding the separate kernel would read --
-// then each thread takes a row and 8 pairs (d, d + hd/2) of one head:
-// q is rotated into the output, k is rotated and v copied into the KV cache
-// at the row's (slot, position), 16 bytes per access.  The k and v columns of
-// the output are not written (attention reads them from the cache).
+// Preproj with the rotary embedding and the KV append fused (the "others" of
+// Sec. 2.1 that follow the QKV matmul).  The rotary pairs are (d, d + hd/2)
+// of a head; so that any tile holds whole pairs, the producers load W's rows
+// in pair order: within each head, logical columns 16g .. 16g+7 are physical
+// columns 8g .. 8g+7 and logical 16g+8 .. 16g+15 are physical hd/2 + 8g ..
+// hd/2 + 8g+7.  Every 16-column group of a tile is then 8 complete pairs of
+// one head of q, k or v (hd a multiple of 16).
+__device__ __forceinline__ int rope_w_row(int n, int N, int hd) {
+  n = min(n, N - 1);
+  const int c = n % hd;
+  return n - c + ((c >> 3) & 1) * (hd / 2) + (c >> 4) * 8 + (c & 7);
+}
+
+// The epilogue: the block's tile goes to LDS as bf16 (the rounding the
+// separate kernel would read); each thread then keeps one 16-column group
+// (one head, 8 frequencies computed once in fp64) and walks rows: q is
+// rotated into the output, k rotated and v copied into the KV cache at the
+// row's (slot, position), 16 bytes per access, both halves of the pairs
+// back at their physical columns.  The k and v columns of the output are not
+// written (attention reads them from the cache).
 template <int BM, int BN, int WGM, int WGN, int WTM, int WTN, int FM, int FN>
 __device__ __forceinline__ void rope_kv_epilogue(const GemmP& p, floatx4 (&acc)[FM][FN], int m0, int n0, int wm,
                                                  int wn, int lane, int tid) {
@@ -268,29 +280,32 @@ __device__ __forceinline__ void rope_kv_epilogue(const GemmP& p, floatx4 (&acc)[
       for (int fn = 0; fn < FN; ++fn) t[r * BN + wn * WTN + fn * 16 + (lane & 15)] = f2bf(acc[fm][fn][i]);
     }
   lds_read_barrier();                                       // the producers pass their last barrier too
+  constexpr int JG = BN / 16;                               // 16-column groups per tile row
+  constexpr int RS = (64 * WGM * WGN) / JG;                 // rows in flight
+  static_assert(BN % 16 == 0 && RS > 0, "16-column groups");
+  const int j = tid % JG, r0 = tid / JG;
+  const int n = n0 + 16 * j;
+  if (r0 >= RS || n >= p.N) return;
   const RopeArgs& a = p.rope;
   const int hd = a.hd, half = hd / 2, QD = a.nh * hd;
-  const int part = n0 / QD;                                 // 0 q, 1 k, 2 v
-  const int groups = half / 8;                              // 8-pair groups per head
-  const int heads = BN / hd;
-  const double lb = log2((double)a.base);
-  bf16* cache = reinterpret_cast<bf16*>(a.kv_layer);
-  // the thread's group g = tid % groups is the same for all its items (the
-  // stride is a multiple of groups): its 8 frequencies are computed once
-  static_assert((64 * WGM * WGN) % 8 == 0, "item stride");
+  const int part = n / QD, head = (n % QD) / hd;            // part 0 q, 1 k, 2 v
+  const int d0 = (n % hd) / 2;                              // first pair of the group
+  const bool rot = part < 2 && a.rope;
   double theta[8];
+  if (rot) {
+    const double lb = log2((double)a.base);
 #pragma unroll
-  for (int e = 0; e < 8; ++e) theta[e] = rope_theta((tid % groups) * 8 + e, hd, lb);
-  for (int it = tid; it < BM * heads * groups; it += 64 * WGM * WGN) {
-    const int g = it % groups, j = (it / groups) % heads, r = it / (groups * heads);
+    for (int e = 0; e < 8; ++e) theta[e] = rope_theta(d0 + e, hd, lb);
+  }
+  bf16* cache = reinterpret_cast<bf16*>(a.kv_layer);
+  const size_t kv_off = (part == 2 ? a.st.kv : 0) + (size_t)head * a.st.head;
+  for (int r = r0; r < BM; r += RS) {
     const int row = m0 + r;
-    if (row >= p.M) continue;
-    const int d0 = g * 8, col = n0 + j * hd;                // first column of the head in [0, 3 QD)
-    const int head = (col % QD) / hd;
-    uint4 lo = *reinterpret_cast<const uint4*>(t + r * BN + j * hd + d0);
-    uint4 hi = *reinterpret_cast<const uint4*>(t + r * BN + j * hd + half + d0);
+    if (row >= p.M) break;
+    uint4 lo = *reinterpret_cast<const uint4*>(t + r * BN + 16 * j);
+    uint4 hi = *reinterpret_cast<const uint4*>(t + r * BN + 16 * j + 8);
     const int slot = a.row_slot[row], pos = a.row_pos[row];
-    if (part < 2 && a.rope) {
+    if (rot) {
       float x0[8], x1[8];
       Vec16<bf16>::unpack(lo, x0);
       Vec16<bf16>::unpack(hi, x1);
@@ -308,13 +323,8 @@ __device__ __forceinline__ void rope_kv_epilogue(const GemmP& p, floatx4 (&acc)[
       lo = make_uint4(w0[0], w0[1], w0[2], w0[3]);
       hi = make_uint4(w1[0], w1[1], w1[2], w1[3]);
     }
-    bf16* dst;
-    if (part == 0) {
-      dst = reinterpret_cast<bf16*>(p.out) + (size_t)row * p.N + col;
-    } else {
-      dst = cache + (size_t)slot * a.st.slot + (part == 2 ? a.st.kv : 0) + (size_t)head * a.st.head +
-            (size_t)pos * a.st.pos;
-    }
+    bf16* dst = part == 0 ? reinterpret_cast<bf16*>(p.out) + (size_t)row * p.N + (n - n % hd)
+                          : cache + (size_t)slot * a.st.slot + kv_off + (size_t)pos * a.st.pos;
     *reinterpret_cast<uint4*>(dst + d0) = lo;
     *reinterpret_cast<uint4*>(dst + half + d0) = hi;
   }
@@ -332,6 +342,7 @@ __global__ __launch_bounds__(64 * (WGM * WGN + NP)) void gemm_ws_kernel(GemmP p)
   static_assert(BM % 8 == 0 && BN % 8 == 0 && ILO > 0, "8-row groups");
   static_assert(WTM % 16 == 0 && WTN % 16 == 0 && (EPI != EPI_SWIGLU || FN % 2 == 0), "wave tile");
   static_assert((S - 2) * IHI < 64 && S >= 2, "stages");
+  static_assert(BM * BN * 2 <= S * ROWS * 128, "the RoPE epilogue stages the bf16 tile in the ring's LDS");
   extern __shared__ uint4 lds[];                 // [S][ROWS * 8] 16-byte chunks
 
   const int per = gridDim.x / 8;
@@ -364,7 +375,10 @@ __global__ __launch_bounds__(64 * (WGM * WGN + NP)) void gemm_ws_kernel(GemmP p)
     for (int j = 0; j < IHI; ++j) {
       const int g = min(j * NP + q, G - 1);
       const int row = g * 8 + (lane >> 3);
-      const size_t r = g < GA ? (size_t)min(m0 + row, p.M - 1) : (size_t)w_row_of<EPI, WTN>(row - BM, n0_out, p.N);
+      const int nl = row - BM;
+      const size_t r = g < GA                  ? (size_t)min(m0 + row, p.M - 1)
+                       : EPI == EPI_ROPE_KV ? (size_t)rope_w_row(n0_out + nl, p.N, p.rope.hd)
+                                            : (size_t)w_row_of<EPI, WTN>(nl, n0_out, p.N);
       off[j] = (uint32_t)(r * p.K * 2 + lchunk * 16);
     }
     const bool extra = q < RHI;
@@ -812,11 +826,11 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s, int forc
   const int out_per_tile = swiglu ? BN / 2 : BN;
   p.tiles_m = (a.M + BM - 1) / BM;
   p.tiles_n = (a.N + out_per_tile - 1) / out_per_tile;
-  // preproj with the rotary embedding and KV append in its epilogue when a
-  // block holds whole heads of one of q, k, v
+  // preproj with the rotary embedding and KV append in its epilogue (W rows
+  // loaded in rotary-pair order, any tile)
   if (ws && a.kind == LIN_PLAIN && a.rope != nullptr) {
     const int hd = a.rope->hd, QD = a.rope->nh * hd;
-    if (BN % hd == 0 && QD % BN == 0 && a.N == 3 * QD) {
+    if (hd % 16 == 0 && a.N == 3 * QD) {
       epi = EPI_ROPE_KV;
       p.rope = *a.rope;
       if (a.rope_done) *a.rope_done = true;
