@@ -23,8 +23,7 @@ through the C-ABI:
 * a tile sweep of the four linear ops of a workload's layer: every
   producer/consumer tile shape (and, for the residual ops, the split-K count
   the planner would use) timed alone through sarathi_linear_tiled, next to
-  the planner's pick; preproj tiles that hold whole heads (the ones whose
-  epilogue can take the rotary embedding and the KV append) are marked.
+  the planner's pick.
 
 Inputs are seeded synthetic tensors drawn on the device (weights
 0.02 * N(0,1), activations and cached K/V N(0,1)); only timing is measured
@@ -412,8 +411,7 @@ def tile_sweep(shape, T: int, iters: int = 20) -> List[dict]:
                 run()
             ms = _time(run, iters)
             out.append({"op": name, "T": T, "N": N, "K": K, "bm": pick[0], "bn": pick[1], "n_split": pick[2],
-                        "us": ms * 1e3, "tflops": 2.0 * T * w_rows * K / (ms * 1e-3) / 1e12, "picked": True,
-                        "whole_heads": False})
+                        "us": ms * 1e3, "tflops": 2.0 * T * w_rows * K / (ms * 1e-3) / 1e12, "picked": True})
             del x, w, resid, y
             continue
         for tile in range(S.sarathi_linear_tile_count()):
@@ -428,8 +426,7 @@ def tile_sweep(shape, T: int, iters: int = 20) -> List[dict]:
                 ms = _time(run, iters)
                 out.append({"op": name, "T": T, "N": N, "K": K, "bm": bm, "bn": bn, "n_split": ns, "us": ms * 1e3,
                             "tflops": 2.0 * T * w_rows * K / (ms * 1e-3) / 1e12,
-                            "picked": (bm, bn, ns) == tuple(pick),
-                            "whole_heads": name == "preproj" and bn % d == 0 and QD % bn == 0})
+                            "picked": (bm, bn, ns) == tuple(pick)})
         del x, w, resid, y
     return out
 
@@ -438,11 +435,11 @@ def tile_sweep_markdown(workload: str, rows: List[dict]) -> str:
     lines = [f"## Linear-op tile sweep: {workload} (T = {rows[0]['T']} rows)\n",
              "Each op alone through `sarathi_linear_tiled` (split-K reductions included), mean of 20 calls after "
              "3 warm-ups; weights re-read every call (a 256 MB memory-side cache can hold one "
-             "op's weights between calls, so these times can be below the in-layer ones).  * = the planner's "
-             "pick; h = a preproj tile that holds whole heads (its epilogue can take RoPE + KV append).\n",
+             "op's weights between calls, so these times can be below the in-layer ones); preproj without its "
+             "RoPE + KV-append epilogue.  * = the planner's pick.\n",
              "| op | N x K | tile (BM x BN) | K-splits | us | TFLOP/s | |", "|---|---|---|---|---|---|---|"]
     for e in rows:
-        mark = ("*" if e["picked"] else "") + ("h" if e["whole_heads"] else "")
+        mark = "*" if e["picked"] else ""
         lines.append(f"| {e['op']} | {e['N']} x {e['K']} | {e['bm']} x {e['bn']} | {e['n_split']} | {e['us']:.1f} | "
                      f"{e['tflops']:.0f} | {mark} |")
     return "\n".join(lines) + "\n"

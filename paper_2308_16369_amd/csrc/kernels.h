@@ -63,7 +63,8 @@ struct LinearArgs {
   float* parts;         // residual kinds: fp32 scratch for split-K partials (null: no split-K)
   size_t parts_cap;     // its capacity in floats
   // LIN_PLAIN preproj (bf16), optional: rotary embedding + KV append fused
-  // into the epilogue when the tile shape allows it (then *rope_done = true,
+  // into the epilogue when head_dim is a multiple of 16 and N = 3 nh hd
+  // (producer/consumer kernel; then *rope_done = true,
   // only the q columns of out are written; else the caller runs
   // launch_rope_append).
   const RopeArgs* rope;
