@@ -451,7 +451,7 @@ int layer_body(const Ctx& c, const sarathi_layer_weights* w, int layer, const vo
   if (e != hipSuccess) return hip_fail(e, "norm_1");
 
   // preproj over all rows, with the rotary embedding and the in-place KV
-  // append in its epilogue when the tile holds whole heads
+  // append in its epilogue (bf16)
   SARATHI_MARK();
   RopeArgs ra{};
   ra.qkv = ws + c.L.qkv; ra.T = T; ra.nh = nh; ra.hd = hd; ra.rope = cfg->rope; ra.base = cfg->rope_base;
