@@ -244,6 +244,31 @@ def test_layer_head_dim_128_tiny_bf16():
     run_and_check(wl.make_instance(shape, b, max_seq_len=512, n_slots=4, seed=5), "hd128 tiny bf16")
 
 
+# (heads, head_dim, chunk rows, decodes, preproj tile the planner picks): the
+# fused RoPE + KV-append epilogue on every producer/consumer tile width,
+# including tiles that cut heads (BN 192 and 224 against 128-wide heads) and
+# a ragged last column tile
+ROPE_TILES = [(40, 128, 4, 4, (64, 64)), (52, 128, 5, 3, (64, 128)), (52, 128, 66, 4, (96, 128)),
+              (52, 128, 96, 4, (96, 192)), (52, 128, 190, 10, (160, 192)), (52, 128, 330, 10, (160, 256)),
+              (52, 128, 790, 10, (160, 224)), (104, 64, 790, 10, (160, 224))]
+
+
+@pytest.mark.parametrize("nh,hd,C,B,tile", ROPE_TILES)
+def test_layer_rope_epilogue_every_tile(nh, hd, C, B, tile):
+    """q, k_new and v_new from preproj's fused rotary + KV-append epilogue
+    against the oracle, on wide-QKV layers whose row counts make the planner
+    pick each tile shape."""
+    # the FFN about as wide as the attention output, so that y - hres (the FFN
+    # output) is not small beside the error that postproj's long sum puts on h
+    shape = _tiny_shape("bf16", hidden=512, n_heads=nh, head_dim=hd, ffn=4096)
+    T = C + B
+    assert tuple(S.sarathi_linear_plan(S.BF16, S.LINEAR_PLAIN, T, 3 * nh * hd, 512, 0)[:2]) == tile
+    b = wl.Batch(prefill_slot=0, chunk_offset=17, chunk_len=C, decode_slots=np.arange(1, B + 1, dtype=np.int32),
+                 decode_ctx=np.array([(53 * i) % 1000 for i in range(1, B + 1)], np.int32))
+    run_and_check(wl.make_instance(shape, b, max_seq_len=1024, n_slots=B + 1, seed=23),
+                  f"rope epilogue nh={nh} hd={hd} T={T} tile={tile}")
+
+
 @pytest.mark.parametrize("dtype,hidden,norm", [("bf16", 24576, "rms"), ("bf16", 12296, "layer"), ("bf16", 4104, "rms"),
                                                ("f32", 12288, "layer"), ("f32", 1032, "rms")])
 def test_layer_wide_hidden(dtype, hidden, norm):
