@@ -319,3 +319,26 @@ def test_attention_plan_counts_partials():
     assert p["partial_rows_read"] == p["partial_rows_written"] and p["combine_rows"] == 101
     with pytest.raises(S.SarathiError):
         S.sarathi_attention_plan(cfg, S.make_batch(-1, 0, 0, [], [])[0])
+
+
+def test_attention_plan_block_size():
+    """The plan prices 256-query blocks (8 waves) and 128-query blocks (4
+    waves, 0.82 of the time per key tile) with the same model -- rounds of
+    256 blocks x (largest key range + 4 tiles) -- and takes the cheaper."""
+    from paper_2308_16369_amd import sarathi as S
+    # LLaMA-13B, chunk 256 @ 512: 256-query blocks: 12 tiles in ranges of 4
+    # (120 blocks, cost 8); 128-query blocks: 10 and 12 tiles in ranges of at
+    # most 4 (240 blocks, cost 8 x 0.82) -> 2 blocks x 3 ranges per head
+    cfg = S.make_cfg(hidden=5120, n_heads=40, head_dim=128, ffn=13824, n_layers=1, dtype=S.BF16)
+    bb, keep = S.make_batch(0, 512, 256, [1], [700])
+    p = S.sarathi_attention_plan(cfg, bb)
+    assert p["chunk_items"] == 6
+    assert p["partial_rows_written"] == 3 * 256 + 2
+    # LLaMA-33B, chunk 512 @ 2048: 256-query blocks of 36 and 40 tiles in two
+    # ranges each fit one round (208 blocks, cost 24); 128-query blocks do no
+    # better than 44 x 0.82 -> 2 blocks x 2 ranges per head
+    cfg = S.make_cfg(hidden=6656, n_heads=52, head_dim=128, ffn=17920, n_layers=1, dtype=S.BF16)
+    bb, keep = S.make_batch(0, 2048, 512, [], [])
+    p = S.sarathi_attention_plan(cfg, bb)
+    assert p["chunk_items"] == 4
+    assert p["partial_rows_written"] == 2 * 512 and p["combine_rows"] == 512
