@@ -836,9 +836,6 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s, int forc
       if (a.rope_done) *a.rope_done = true;
     }
   }
-  // rotated k order pays off for two M-tiles over 128-row W panels (measured:
-  // -13% on preproj at 320 rows; no gain with 256-row panels or four M-tiles)
-  p.rotate_k = (ws && BN == 128 && p.tiles_m == 2) ? 1 : 0;
 
   // Split-K for the residual ops when the tile grid leaves CUs idle: every
   // split stores its fp32 partial, then one pass adds residual + partials in
@@ -863,6 +860,15 @@ hipError_t launch_linear(int dtype, const LinearArgs& a, hipStream_t s, int forc
     }
   }
   p.n_tiles = p.tiles_m * p.tiles_n * p.n_split;
+  // Rotated k order for the two M-tiles of a W panel, when a block runs at
+  // most 192 k-tiles.  Measured in the layers: LLaMA-13B preproj -13% and
+  // ffn_ln1 -2%; LLaMA-33B at 288 rows every op -2..-5% (layer -4%); GPT-3
+  // preproj, postproj and ffn_ln1 -2..-6% (96-192 k-tiles); but GPT-3 ffn_ln2
+  // (384 k-tiles per split) +6%.  Four M-tiles: no gain.
+  {
+    const int nk_block = (n_split > 1 ? p.k_split : a.K) / 64;
+    p.rotate_k = (ws && p.tiles_m == 2 && nk_block <= 192) ? 1 : 0;
+  }
   if (plan) {
     *plan = LinearPlan{BM, BN, p.n_split};
     return hipSuccess;
