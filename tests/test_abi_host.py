@@ -321,6 +321,38 @@ def test_attention_plan_counts_partials():
         S.sarathi_attention_plan(cfg, S.make_batch(-1, 0, 0, [], [])[0])
 
 
+def test_attention_plan_invariants_random():
+    """On random single-chunk batches (several head counts, chunk lengths,
+    prefixes and decode contexts) the plan's counts are consistent: one
+    decode item per 512-key split; every partial row written is read back
+    once; the combine pass covers the decodes plus exactly the chunk rows
+    whose query block was split; a prefix-plus-chunk of at most four key
+    tiles is never split; the chunk items cover every query block."""
+    import random
+    from paper_2308_16369_amd import sarathi as S
+    rng = random.Random(2308)
+    for nh in (8, 40, 52, 96):
+        cfg = S.make_cfg(hidden=nh * 128, n_heads=nh, head_dim=128, ffn=4 * nh * 128, n_layers=1, dtype=S.BF16)
+        for _ in range(60):
+            C = rng.choice([0, 1, rng.randint(2, 127), 128, rng.randint(129, 600), rng.randint(600, 2048)])
+            off = rng.choice([0, rng.randint(1, 300), rng.randint(300, 20000)]) if C else 0
+            B = rng.randint(0 if C else 1, 40)
+            ctx = [rng.randint(0, 5000) for _ in range(B)]
+            bb, keep = S.make_batch(0 if C else -1, off, C, list(range(1, B + 1)), ctx)
+            p = S.sarathi_attention_plan(cfg, bb)
+            assert p["decode_items"] == sum((c + 1 + 511) // 512 for c in ctx)
+            assert p["partial_rows_written"] == p["partial_rows_read"]
+            chunk_partials = p["partial_rows_written"] - p["decode_items"]
+            split_rows = p["combine_rows"] - B
+            assert 0 <= split_rows <= C and chunk_partials >= 2 * split_rows
+            if off + C <= 256:
+                assert chunk_partials == 0 and split_rows == 0
+            if C:
+                assert -(-C // 256) <= p["chunk_items"] <= -(-C // 128) * -(-(off + C) // 256)
+            else:
+                assert p["chunk_items"] == 0
+
+
 def test_attention_plan_block_size():
     """The plan prices 256-query blocks (8 waves) and 128-query blocks (4
     waves, 0.82 of the time per key tile) with the same model -- rounds of
