@@ -45,6 +45,8 @@ def parse():
     ap.add_argument("--no-stack", action="store_true",
                     help="skip the 40-layer model-step measurement (the 'stack' object)")
     ap.add_argument("--stack-steps", type=int, default=5)
+    ap.add_argument("--stack-only", action="store_true",
+                    help="measure only the 40-layer model step and print its object (for kernel traces of it)")
     return ap.parse_args()
 
 
@@ -339,6 +341,9 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.stack_only:
+        print(json.dumps(bench_stack(args.stack_steps, 2, cpu_baseline=not args.no_cpu_baseline)), flush=True)
+        return
     w = wl.WORKLOADS[args.workload]
     shp = w.shape
     t0 = time.time()
